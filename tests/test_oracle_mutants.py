@@ -1,0 +1,92 @@
+"""Plant plausible mistakes into copies of the oracle (on the CPU) and check
+that the pins catch every one of them.
+
+Each mutant is one textual edit of ``oracle/recache_oracle.c``: a sign, a
+dropped term, a wrong index, a transposed operand or an off-by-one.  The
+mutated copy is compiled into a temporary directory, swapped in for the real
+library, and the pin tests run against it; at least one must fail.
+"""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "recache_oracle.c")
+
+MUTANTS = {
+    "rope_sign": ("y[i] = a * c - b * s;", "y[i] = a * c + b * s;"),
+    "rope_second_half_sign": ("y[i + half] = b * c + a * s;", "y[i + half] = b * c - a * s;"),
+    "rope_freq_exponent": ("pow(base, -2.0 * (double)i / (double)d)",
+                           "pow(base, -1.0 * (double)i / (double)d)"),
+    "rope_interleaved_pairs": ("double a = x[i], b = x[i + half];",
+                               "double a = x[(2 * i) % d], b = x[(2 * i + 1) % d];"),
+    "encode_no_local_reset": ("double p = (double)((pos_base ? pos_base[r] : 0) + (t - cu_len[r]));",
+                              "double p = (double)((pos_base ? pos_base[r] : 0) + t);"),
+    "encode_drops_diagonal": ("for (int u = 0; u <= j; ++u) {",
+                              "for (int u = 0; u <= j - (j > 0); ++u) {"),
+    "scale_dropped_encode": ("z[u] = scale * dot;\n            }\n            struct enc_vctx",
+                             "z[u] = dot;\n            }\n            struct enc_vctx"),
+    "scale_dropped_attend": ("z[u] = scale * dot;\n            }\n            struct att_vctx",
+                             "z[u] = dot;\n            }\n            struct att_vctx"),
+    "gqa_modulo": ("int s = (int)(sh / Hq), h = (int)(sh % Hq), g = h / ratio;",
+                   "int s = (int)(sh / Hq), h = (int)(sh % Hq), g = h % Hkv;"),
+    "lse_without_max": ("return m + log(denom);", "return log(denom);"),
+    "causal_top_left": ("int last_ctx = Tc - Tq + i;", "int last_ctx = i;"),
+    "mask_index_transposed": ("if (!mask[((size_t)r * n_layers + layer) * Hkv + g]) continue;",
+                              "if (!mask[((size_t)r * Hkv + g) * n_layers + layer]) continue;"),
+    "kept_ignored": ("key_row[n++] = (int64_t)cu_rows[r] + kept_idx[t];",
+                     "key_row[n++] = (int64_t)cu_rows[r] + (t - cu_kept[r]);"),
+    "prune_wrong_source": ("size_t src = ((size_t)g * T + cu_len[r] + kept_idx[j]) * row;",
+                           "size_t src = ((size_t)g * T + cu_len[r] + j - cu_kept[r]) * row;"),
+    "routes_count_resources": ("tokens += cu_kept[r + 1] - cu_kept[r];", "tokens += 1;"),
+    "routes_skip_mask": ("if (mask[((size_t)r * L + l) * G + g]) {", "if (1) {"),
+    "vcache_from_k": ("v_cache[((size_t)g * T + t) * d + e] = widen(v, dtype,",
+                      "v_cache[((size_t)g * T + t) * d + e] = widen(k, dtype,"),
+    "softmax_no_normalise": ("for (int e = 0; e < d; ++e) out[e] /= denom;", ""),
+}
+
+PINS = [
+    pins.test_rope_d2_closed_form,
+    pins.test_rope_matches_complex_form_and_identities,
+    pins.test_encode_single_resource_is_textbook_causal_attention,
+    pins.test_encode_blockdiag_matches_bruteforce_and_lse,
+    pins.test_encode_first_token_is_its_value_row,
+    pins.test_encode_zero_queries_give_running_mean,
+    lambda: pins.test_attend_matches_bruteforce_final_mask(3),
+    lambda: pins.test_attend_matches_bruteforce_final_mask(4),
+    pins.test_attend_all_ones_mask_is_causal_over_concatenation,
+    pins.test_attend_all_zeros_mask_is_context_only,
+    pins.test_attend_decode_row_sees_every_context_row,
+    pins.test_prune_matches_fancy_indexing_and_extremes,
+    pins.test_routes_match_python_loops,
+]
+
+
+@pytest.fixture(scope="module")
+def source():
+    oracle._load()
+    with open(SRC) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, source, tmp_path, monkeypatch):
+    old, new = MUTANTS[name]
+    assert source.count(old) == 1, "mutation target not found exactly once: %r" % old
+    path = tmp_path / ("m_%s.c" % name)
+    path.write_text(source.replace(old, new))
+    so = tmp_path / ("m_%s.so" % name)
+    subprocess.check_call(["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-w",
+                           "-o", str(so), str(path), "-lm"])
+    monkeypatch.setattr(oracle, "_lib", ctypes.CDLL(str(so)))
+    caught = []
+    for pin in PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError):
+            caught.append(getattr(pin, "__name__", "lambda"))
+    assert caught, "mutant %s survived every pin" % name
