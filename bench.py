@@ -1,0 +1,331 @@
+"""Benchmark of the resource-wise attention hot path on one MI355X.
+
+Headline workload (one JSON line): resource encoding prefill at the Qwen3-4B
+attention shape -- one layer, 16 packed resources with lengths U[200, 1500],
+32 query / 8 KV heads, head_dim 128, bf16, RoPE base 1e6.  One step is the
+whole path this workload defines: RoPE of K at resource-local positions with
+the head-major K/V cache write, then block-diagonal causal attention with the
+query RoPE fused in.  value = effective TFLOP/s = 4 * head_dim * n_q_heads *
+sum_i D_i (D_i + 1) / 2 per step / step time (unmasked pairs only).
+
+The same run also measures the other hot-path steps on their own workloads
+("rows"): kept-row gather, route build, conversation prefill over all routes
+(36 layers, 8 requests x 2048 tokens over 8 resources each), the pruned
+variant (25% of routes, 30% of tokens), and batched decode (36 layers, 64
+requests over 32 resources each plus 4096 context rows).
+
+Inputs are synthetic (seeded N(0, 1) tensors, see workloads.py) and resident
+in HBM before timing starts.  The CPU baseline is the fp64 oracle on the
+headline workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+METRIC = "effective attention TFLOP/s (prefill) & HBM GB/s (decode), % of MI355X peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def i32(a, dev):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, np.int32))).to(dev)
+
+
+def encode_flops(w) -> float:
+    return 4.0 * w.head_dim * w.n_q_heads * w.pairs_per_head()
+
+
+def headline(args, dev):
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config
+
+    w = config(2)["encode"]
+    T, Hq, Hkv, d = w.total, w.n_q_heads, w.n_kv_heads, w.head_dim
+    q, k, v = w.tensors(dev)
+    cu = i32(w.cu_len, dev)
+    pos = i32(np.concatenate([np.arange(n) for n in w.lengths]), dev)  # resource-local positions
+    out = torch.empty_like(q)
+    kc = torch.empty(Hkv, T, d, dtype=q.dtype, device=dev)
+    vc = torch.empty_like(kc)
+    max_len = int(w.lengths.max())
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        if evs:
+            evs[0].record(stream)
+        rc.rope_kv(k, v, pos, w.rope_base, kc, vc)
+        if evs:
+            evs[1].record(stream)
+        rc.encode_attention(q, kc, vc, cu, max_len, w.rope_base, out)
+        if evs:
+            evs[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    attn_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    rope_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    flops = encode_flops(w)
+    ms = wall * 1e3 / args.steps
+    return w, {
+        "flops": flops, "ms_per_step": ms, "tflops": flops / (ms * 1e-3) / 1e12,
+        "attn_ms": attn_ms, "rope_ms": rope_ms, "tokens": T,
+        "pairs_per_head": w.pairs_per_head(),
+    }, (q, k, v)
+
+
+def timed(fn, reps, warm=1):
+    import torch
+
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        fn()
+    b.record(s)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def visible_tokens(w):
+    """S_vis[b][l][g]: kept rows of b's resources whose route (l, g) is set."""
+    kl = w.kept_lengths.astype(np.int64)
+    s = np.zeros((w.n_req, w.n_layers, w.n_kv_heads), np.int64)
+    for b in range(w.n_req):
+        rs = w.req_res[w.req_res_off[b]:w.req_res_off[b + 1]]
+        s[b] = np.einsum("r,rlg->lg", kl[rs], w.mask[rs].astype(np.int64))
+    return s
+
+
+def prefill_row(k, dev, reps):
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config
+
+    w = config(k)["attend"]
+    L, G, r = w.n_layers, w.n_kv_heads, w.n_q_heads // w.n_kv_heads
+    s_vis = visible_tokens(w)
+    tq = w.q_lens.astype(np.int64)[:, None, None]
+    tc = w.ctx_lens.astype(np.int64)[:, None, None]
+    pairs = tq * s_vis + tq * (tq + 1) // 2 + tq * (tc - tq)
+    flops = 4.0 * w.head_dim * r * float(pairs.sum())
+    layers = [w.layer_tensors(l, dev) for l in range(L)]
+    outs = [torch.empty_like(t[0]) for t in layers]
+    st = _routes(w, dev)
+
+    def run():
+        for l in range(L):
+            q, ck, cv, rk, rv = layers[l]
+            rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], int(w.q_lens.max()),
+                             int(w.ctx_lens.max()), rk, rv, st["cu_rows"], st["route_off"],
+                             st["route_res"], st["route_tokens"], l, L, outs[l],
+                             max_route_len=st["max_route_len"])
+
+    ms = timed(run, reps)
+    res = {"workload": "config %d" % k, "layers": L, "ms_per_pass": ms,
+           "tflops": flops / (ms * 1e-3) / 1e12, "flops": flops}
+    res["pct_of_peak"] = 100.0 * res["tflops"] / PEAK_BF16_TFLOPS
+    del layers, outs
+    torch.cuda.empty_cache()
+    return res
+
+
+def _routes(w, dev):
+    import torch
+    from paper_2608_19662_amd import recache as rc
+
+    E = w.n_req * w.n_layers * w.n_kv_heads
+    st = {"cu_q": i32(w.cu_q, dev), "cu_ctx": i32(w.cu_ctx, dev), "cu_rows": i32(w.cu_rows, dev),
+          "route_off": torch.empty(E + 1, dtype=torch.int32, device=dev),
+          "route_res": torch.empty(int(w.req_res_off[-1]) * w.n_layers * w.n_kv_heads,
+                                   dtype=torch.int32, device=dev),
+          "route_tokens": torch.empty(E, dtype=torch.int32, device=dev),
+          "max_route_len": int(np.diff(w.req_res_off).max())}
+    st["args"] = (i32(w.req_res_off, dev), i32(w.req_res, dev),
+                  torch.from_numpy(w.mask).to(dev), st["cu_rows"], st["route_off"],
+                  st["route_res"], st["route_tokens"])
+    rc.build_routes(*st["args"])
+    return st
+
+
+def decode_row(dev, reps):
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config
+
+    w = config(5)["attend"]
+    L, G, d = w.n_layers, w.n_kv_heads, w.head_dim
+    s_vis = visible_tokens(w)
+    keys = s_vis + w.ctx_lens.astype(np.int64)[:, None, None]
+    kv_bytes = float(keys.sum()) * 2 * d * 2
+    qo_bytes = 2.0 * L * w.n_req * w.n_q_heads * d * 2
+    max_kv = int(keys.max())
+    layers = []
+    for l in range(L):
+        layers.append(w.layer_tensors(l, dev))
+    outs = [torch.empty_like(t[0]) for t in layers]
+    st = _routes(w, dev)
+    nb = rc.attend_workspace_bytes(w.n_req, 1, int(w.ctx_lens.max()), max_kv, w.n_q_heads, G, d)
+    ws = torch.empty(nb // 4, dtype=torch.float32, device=dev)
+
+    def run():
+        for l in range(L):
+            q, ck, cv, rk, rv = layers[l]
+            rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], 1, int(w.ctx_lens.max()), rk, rv,
+                             st["cu_rows"], st["route_off"], st["route_res"], st["route_tokens"], l,
+                             L, outs[l], workspace=ws, max_kv=max_kv,
+                             max_route_len=st["max_route_len"])
+
+    ms = timed(run, reps)
+    gbs = (kv_bytes + qo_bytes) / (ms * 1e-3) / 1e9
+    route_ms = timed(lambda: rc.build_routes(*st["args"]), reps)
+    res = {"workload": "config 5", "layers": L, "ms_per_step": ms, "gbs": gbs,
+           "pct_of_peak": 100.0 * gbs / PEAK_HBM_GBS, "bytes": kv_bytes + qo_bytes,
+           "resident_gb": sum(t.numel() * t.element_size() for lt in layers for t in lt) / 1e9}
+    del layers, outs
+    torch.cuda.empty_cache()
+    return res, {"workload": "config 5 (64 req x 36 layers x 8 groups)", "ms": route_ms,
+                 "entries": int(w.n_req * L * G)}
+
+
+def prune_row(dev, reps):
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config, normal
+
+    w = config(4)["attend"]
+    T, K, d = int(w.cu_len[-1]), int(w.cu_kept[-1]), w.head_dim
+    kc = normal((8, T, d), torch.bfloat16, 4, 900, dev)
+    vc = normal((8, T, d), torch.bfloat16, 4, 901, dev)
+    kk = torch.empty(8, K, d, dtype=torch.bfloat16, device=dev)
+    vk = torch.empty_like(kk)
+    a = (i32(w.cu_len, dev), i32(w.cu_kept, dev), i32(w.kept_idx, dev))
+    ms = timed(lambda: rc.prune_gather(kc, vc, *a, kk, vk), reps)
+    nbytes = 2.0 * 2 * 8 * K * d * 2  # read + write of K and V kept rows
+    return {"workload": "config 4, one layer", "ms": ms, "gbs": nbytes / (ms * 1e-3) / 1e9,
+            "pct_of_peak": 100.0 * nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, "rows_kept": K}
+
+
+def cpu_baseline(w, tensors):
+    """The fp64 oracle on the headline workload (all 16 resources, one pass)."""
+    import oracle
+
+    q, k, v = (t.cpu() for t in tensors)
+    t0 = time.perf_counter()
+    oracle.encode(q, k, v, w.cu_len, w.rope_base)
+    dt = time.perf_counter() - t0
+    return {"value": encode_flops(w) / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle", "seconds": dt,
+            "sample": "full config 2 workload (16 resources, one layer), one pass, fp64"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--rows", default="all", help="extra hot-path rows: all | none")
+    ap.add_argument("--reps", type=int, default=5, help="repetitions per extra row")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(sharding is design-only); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    log("headline: config 2 encode, %d warmup + %d steps" % (args.warmup, args.steps))
+    w, h, tensors = headline(args, dev)
+    log("headline done: %.3f ms/step, %.1f TFLOP/s (attention kernel %.3f ms, rope %.3f ms)" % (
+        h["ms_per_step"], h["tflops"], h["attn_ms"], h["rope_ms"]))
+    achieved = h["flops"] / (h["attn_ms"] * 1e-3) / 1e12
+    traffic = None
+    rows = {}
+    if args.rows != "none":
+        del tensors
+        torch.cuda.empty_cache()
+        for name, fn in (("a4_prune_gather", lambda: prune_row(dev, args.reps)),
+                         ("a6_prefill_config3", lambda: prefill_row(3, dev, args.reps)),
+                         ("a6_prefill_config4", lambda: prefill_row(4, dev, args.reps))):
+            log("row", name)
+            rows[name] = fn()
+            log("  ", json.dumps(rows[name]))
+        log("row a7_decode_config5 + a5_route_build")
+        rows["a7_decode_config5"], rows["a5_route_build"] = decode_row(dev, args.reps)
+        log("  ", json.dumps(rows["a7_decode_config5"]))
+        tensors = w.tensors(dev)
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(w, tensors)
+        log("  ", json.dumps(cpu))
+    line = {
+        "metric": METRIC,
+        "value": round(h["tflops"], 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "config 2: resource encoding prefill, 1 layer, 16 packed resources "
+                        "U[200,1500] (%d tokens), 32 q / 8 KV heads, head_dim 128, bf16, "
+                        "resource-local RoPE base 1e6" % h["tokens"],
+            "pairs_per_head": h["pairs_per_head"],
+            "flops_per_step": h["flops"],
+            "step": "rope_kv (resource-local positions, head-major cache write) + "
+                    "block-diagonal causal attention with fused query RoPE",
+        },
+        "pct_of_peak": round(100.0 * h["tflops"] / PEAK_BF16_TFLOPS, 2),
+        "roofline": {
+            "kernel": "attn_mfma_kernel<128, encode>",
+            "bound": "mfma",
+            "achieved": round(achieved, 3),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "avg_kernel_ms": round(h["attn_ms"], 5),
+        },
+        "cpu_baseline": cpu,
+        "rows": rows,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

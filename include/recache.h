@@ -1,0 +1,235 @@
+/*
+ * recache.h -- C ABI of the MI355X (gfx950) resource-wise attention library.
+ *
+ * ReCache (arXiv 2608.19662) encodes each retrieved resource (a tool or skill
+ * schema) as an independent KV block and lets conversation tokens read those
+ * blocks only through selected (layer, KV group) routes and only at retained
+ * token positions.  This library implements that data path on one GPU:
+ *
+ *   recache_rope_q / recache_rope_kv   RoPE at explicit positions; K/V cache write
+ *   recache_encode_resources           block-diagonal causal encode (Sec. 3,
+ *                                      "Resource-Wise Attention"; Fig. 2(a))
+ *   recache_encode_attention           its attention half, on built caches
+ *   recache_prune_gather               kept-token compaction (Sec. 3,
+ *                                      "Semantic Pruning"; Fig. 2(c))
+ *   recache_build_routes               per (request, layer, KV group) visible
+ *                                      resource lists (Sec. 3, "Structural
+ *                                      Pruning"; Fig. 2(b))
+ *   recache_attend_cached              conversation queries over routed, kept
+ *                                      resource rows plus causal context (final
+ *                                      ReCache mask, Fig. 2)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers unless a parameter is marked [host].  The
+ *   caller owns every buffer; the library allocates no device memory, keeps no
+ *   pointer after returning and holds no state besides a thread-local error
+ *   string.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *   device work is enqueued on it; nothing synchronises.
+ * - Scalar arguments are validated on the host before any launch.  On a
+ *   non-zero return no kernel has been launched and no output was written
+ *   (except RECACHE_EHIP, which reports a launch failure).
+ *   recache_last_error() returns the text for the last non-OK status of the
+ *   calling thread.
+ * - Device index arrays (offsets, kept lists, route lists) are trusted by the
+ *   kernels: pass them through recache_check_offsets / recache_check_kept on a
+ *   host copy when they come from an untrusted source.  Kernels clamp every
+ *   address they form to the extents given as scalars, so bad device indices
+ *   give wrong numbers, never accesses outside the buffers.
+ * - Element types: RECACHE_F32 (float) or RECACHE_BF16 (bfloat16); all
+ *   floating tensors of one call share the dtype.  bf16 math accumulates in
+ *   fp32; outputs are rounded to nearest even.  head_dim is 64 or 128.
+ * - Layouts: token-major tensors are [rows][heads][head_dim]; KV caches are
+ *   head-major [kv_heads][cache_rows][head_dim], so the rows of one resource
+ *   (or one request's context) for one KV group are contiguous.  GQA: query
+ *   head h reads KV head h / (n_q_heads / n_kv_heads).
+ * - RoPE pairs element i with element i + head_dim/2 ("rotate half"), with
+ *   theta_i = rope_base^(-2i/head_dim); angles are reduced in fp64.
+ * - softmax_scale <= 0 selects 1/sqrt(head_dim).  LSE outputs are natural-log
+ *   sum-exp of the scaled logits, fp32, [n_q_heads][rows].
+ */
+#ifndef RECACHE_H
+#define RECACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum recache_status {
+    RECACHE_OK = 0,
+    RECACHE_EINVAL = -1,       /* bad argument: null pointer, bad size, Tq > Tc, ... */
+    RECACHE_EUNSUPPORTED = -2, /* valid but not implemented: head_dim, dtype, GQA ratio */
+    RECACHE_EWORKSPACE = -3,   /* workspace missing or smaller than required */
+    RECACHE_EHIP = -4          /* a HIP call failed (launch error, bad device pointer) */
+};
+
+enum recache_dtype { RECACHE_F32 = 0, RECACHE_BF16 = 1 };
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int recache_version(void);
+
+/* Text of the last non-OK status returned on this thread ("" if none). */
+const char* recache_last_error(void);
+
+/*
+ * RoPE in place on x[T][n_heads][head_dim] at positions pos[T] (device int32).
+ * Used for conversation queries, whose positions continue the original
+ * sequence (Sec. 3, "Resource-Wise Attention": the surrounding context keeps
+ * its positional encodings).
+ */
+int recache_rope_q(int dtype, int T, int n_heads, int head_dim, double rope_base,
+                   const int32_t* pos, void* x, void* stream);
+
+/*
+ * Rotate k[T][n_kv_heads][head_dim] at pos[T] and write it to
+ * k_cache[g][row0 + t][:]; copy v[T][n_kv_heads][head_dim] to
+ * v_cache[g][row0 + t][:].  Caches are [n_kv_heads][cache_rows][head_dim];
+ * requires 0 <= row0 and row0 + T <= cache_rows.  Used to append conversation
+ * K/V (context positions) and, inside recache_encode_resources, resource K/V
+ * at resource-local positions.
+ */
+int recache_rope_kv(int dtype, int T, int n_kv_heads, int head_dim, double rope_base,
+                    const int32_t* pos, const void* k, const void* v,
+                    void* k_cache, void* v_cache, int cache_rows, int row0, void* stream);
+
+/*
+ * One layer of resource encoding (Sec. 3, "Resource-Wise Attention";
+ * Fig. 2(a)).  n_res resources are packed in order: resource r owns rows
+ * [cu_len[r], cu_len[r+1]) (device int32, cu_len[0] = 0, every length >= 1,
+ * cu_len[n_res] = total_T, every length <= max_len).  Token j of resource r
+ * gets position pos_base[r] + j (pos_base device int32 [n_res], or NULL for
+ * 0: resource-local positions, pos(t_ij) = j).
+ *
+ * Query row t of resource r, head h, attends keys u in [cu_len[r], t] of KV
+ * head h / (Hq / Hkv) only: no attention crosses resources, so each
+ * resource's outputs and cache rows do not depend on its neighbours or on
+ * its packing offset (bit-exact on the GPU).
+ *
+ *   q[total_T][n_q_heads][head_dim], k/v[total_T][n_kv_heads][head_dim]: inputs
+ *   out[total_T][n_q_heads][head_dim]: attention output
+ *   k_cache/v_cache[n_kv_heads][total_T][head_dim]: rotated K and plain V,
+ *       the resource KV blocks to keep for reuse
+ *   lse[n_q_heads][total_T] (fp32) or NULL
+ */
+int recache_encode_resources(int dtype, int n_res, const int32_t* cu_len, int total_T,
+                             int max_len, int n_q_heads, int n_kv_heads, int head_dim,
+                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             const void* q, const void* k, const void* v, void* out,
+                             void* k_cache, void* v_cache, float* lse, void* stream);
+
+/*
+ * The attention half of recache_encode_resources on caches that already hold
+ * the rotated keys and the values of the packed resources
+ * (k_cache/v_cache[n_kv_heads][total_T][head_dim], e.g. written by
+ * recache_rope_kv at positions pos_base[r] + j).  Queries are rotated on the
+ * fly at the same positions.  Same arguments and outputs otherwise;
+ * recache_encode_resources = recache_rope_kv + this call.
+ */
+int recache_encode_attention(int dtype, int n_res, const int32_t* cu_len, int total_T,
+                             int max_len, int n_q_heads, int n_kv_heads, int head_dim,
+                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             const void* q, const void* k_cache, const void* v_cache, void* out,
+                             float* lse, void* stream);
+
+/*
+ * Semantic-pruning gather, one layer (Sec. 3, "Semantic Pruning"): resource r
+ * keeps local token indices kept_idx[cu_kept[r] .. cu_kept[r+1]) (device
+ * int32, strictly ascending, inside [0, D_r), at least one per resource;
+ * cu_kept[n_res] = total_kept).  Kept rows are copied bit for bit, so they
+ * keep the rotation they got at construction:
+ *   k_kept[g][cu_kept[r] + j] = k_cache[g][cu_len[r] + kept_idx[cu_kept[r] + j]]
+ * and the same for v.  Caches are [n_kv_heads][total_T][head_dim], outputs
+ * [n_kv_heads][total_kept][head_dim].
+ */
+int recache_prune_gather(int dtype, int n_res, const int32_t* cu_len, const int32_t* cu_kept,
+                         const int32_t* kept_idx, int total_T, int total_kept, int n_kv_heads,
+                         int head_dim, const void* k_cache, const void* v_cache, void* k_kept,
+                         void* v_kept, void* stream);
+
+/*
+ * Structural-pruning routes for every (request, layer, KV group) (Sec. 3,
+ * "Structural Pruning"): route_mask[r][l][g] (device uint8, non-zero = the
+ * route (l, g) of resource r is in Omega and exposes its states) generalises
+ * the paper's Omega* = L* x G* to a per-resource mask.  Request b lists
+ * resources req_res[req_res_off[b] .. req_res_off[b+1]) (device int32,
+ * request order, ids in [0, n_res); req_res_off[n_req] = total_req_res).
+ *
+ * For entry e = (b * n_layers + l) * n_kv_heads + g the outputs are
+ *   route_res[route_off[e] .. route_off[e+1]): the listed resources of b whose
+ *       bit (l, g) is set, in request order;
+ *   route_tokens[e]: the sum of their kept lengths, cu_kept[r+1] - cu_kept[r].
+ * route_off has n_req * n_layers * n_kv_heads + 1 entries (route_off[0] = 0);
+ * route_res needs room for total_req_res * n_layers * n_kv_heads ids.
+ * Results are exact and deterministic.
+ */
+int recache_build_routes(int n_req, const int32_t* req_res_off, const int32_t* req_res,
+                         int total_req_res, int n_res, int n_layers, int n_kv_heads,
+                         const uint8_t* route_mask, const int32_t* cu_kept, int32_t* route_off,
+                         int32_t* route_res, int32_t* route_tokens, void* stream);
+
+/*
+ * Workspace bytes that recache_attend_cached needs for these sizes (0 when
+ * max_q > 1: the prefill kernels use none).  max_kv is an upper bound on the
+ * keys a (request, group) can see in one layer (route tokens + context), used
+ * only to size the split-KV decode; 0 means "use max_ctx".
+ */
+size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max_kv,
+                                      int n_q_heads, int n_kv_heads, int head_dim);
+
+/*
+ * Conversation tokens over cached resources, one layer (final ReCache mask,
+ * Fig. 2; Sec. 3, "Structural Pruning" and "Semantic Pruning").
+ *
+ * Request b has Tq_b = cu_q[b+1] - cu_q[b] queries and Tc_b = cu_ctx[b+1] -
+ * cu_ctx[b] context rows, 1 <= Tq_b <= Tc_b <= max_ctx, Tq_b <= max_q,
+ * cu_q[n_req] = total_q; its queries are the last Tq_b context tokens.  For query i of request b, head
+ * h and group g = h / (Hq / Hkv), the visible keys are, in this order:
+ *   1. every kept row of every resource in route_res[route_off[e] ..
+ *      route_off[e+1]) with e = (b * n_layers + layer) * n_kv_heads + g
+ *      (rows res_k[g][cu_kept[r] .. cu_kept[r+1])) -- M_resource routes; an
+ *      empty list is an M_context route;
+ *   2. context rows ctx_k[g][cu_ctx[b] + c] for c = 0 .. Tc_b - Tq_b + i
+ *      (causal, bottom-right aligned; with Tq = 1 the new token sees all).
+ *
+ *   q[total_q][n_q_heads][head_dim]: rotated queries
+ *   ctx_k/ctx_v[n_kv_heads][ctx_rows][head_dim]: rotated context K, context V
+ *   res_k/res_v[n_kv_heads][res_rows][head_dim]: compacted kept rows of this
+ *       layer (output of recache_prune_gather, or unpruned caches with
+ *       cu_kept = cu_len)
+ *   route_off/route_res/route_tokens: output of recache_build_routes
+ *   out[total_q][n_q_heads][head_dim]; lse[n_q_heads][total_q] or NULL
+ *   max_route_len: upper bound on the resources of any route list (at most
+ *       1024), i.e. on resources per request
+ *   workspace: device scratch of recache_attend_workspace_bytes(...) bytes
+ *       (may be NULL when that is 0); contents need no initialisation.
+ */
+int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const int32_t* cu_q,
+                          const int32_t* cu_ctx, int total_q, int max_q, int max_ctx, int max_kv,
+                          int max_route_len, int n_q_heads, int n_kv_heads, int head_dim,
+                          float softmax_scale, const void* q, const void* ctx_k,
+                          const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
+                          int res_rows, const int32_t* cu_kept, const int32_t* route_off,
+                          const int32_t* route_res, const int32_t* route_tokens, void* out,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * [host] Validators for host copies of index arrays.  Return RECACHE_OK or
+ * RECACHE_EINVAL (with recache_last_error() naming the first bad entry).
+ *   recache_check_offsets: cu[0] = 0, cu non-decreasing (strictly increasing
+ *       when strict != 0), cu[n] = total.
+ *   recache_check_kept: for each resource, kept indices strictly ascending,
+ *       inside [0, D_r), at least one, and cu_kept consistent.
+ */
+int recache_check_offsets(const int32_t* cu, int n, int total, int strict);
+int recache_check_kept(const int32_t* cu_len, const int32_t* cu_kept, const int32_t* kept_idx,
+                       int n_res);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RECACHE_H */

@@ -48,6 +48,11 @@ def _load():
     return _lib
 
 
+def threads() -> int:
+    """OpenMP threads the oracle runs on."""
+    return int(_load().oracle_threads())
+
+
 def host_view(t):
     """numpy view of a CPU tensor/array: float32 stays float32, bf16 -> uint16 bits."""
     if isinstance(t, np.ndarray):

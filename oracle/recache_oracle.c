@@ -44,6 +44,7 @@
  * order invariance, and exact index comparisons).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -51,6 +52,9 @@
 #define ORACLE_F32 0
 #define ORACLE_BF16 1
 #define ORACLE_F64 2
+
+/* Threads the OpenMP loops below use. */
+int oracle_threads(void) { return omp_get_max_threads(); }
 
 /* Exact widening of one stored element to double. */
 static double widen(const void* base, int dtype, size_t i) {

@@ -1,0 +1,384 @@
+// bf16 flash attention on gfx950 MFMA, shared by
+//   - resource encoding: block-diagonal causal attention inside each packed
+//     resource, with RoPE at resource-local positions applied to the query
+//     tile on load (ReCache Sec. 3, "Resource-Wise Attention"; Fig. 2(a));
+//   - conversation prefill: queries over the kept rows of the resources routed
+//     to their (layer, KV group), then causal context (final ReCache mask,
+//     Fig. 2; Sec. 3, "Structural Pruning" / "Semantic Pruning").
+//
+// Both are one "key stream" per (unit, KV group): a query with local index i
+// sees stream keys p <= off + i.  Encode: unit = resource, stream = its rows,
+// off = 0.  Prefill: unit = request, stream = [routed kept rows in request
+// order] ++ [context rows], off = S_vis + Tc - Tq.
+//
+// Work decomposition.  A workgroup is 4 waves that share one KV group: it
+// holds up to 4 query heads of the group over 32 query rows (or fewer heads
+// over 64 / 128 rows when the group has fewer heads).  Each wave owns one
+// (head, 32-row block) and computes the transposed products
+//     S^T = K Q^T    (32x32x16 bf16 MFMA; A = K rows from LDS, B = Q^T in VGPRs)
+//     O^T += V^T P^T (A = V^T from LDS, B = P^T straight from the S^T accumulators)
+// so every lane owns exactly one query row in both accumulators: row max and
+// row sum need one cross-lane step (lanes l and l^32), and the rescale of O is
+// lane-local.  K / V tiles of 64 keys are staged through LDS, double buffered
+// (global loads of tile t+1 are in flight while tile t is computed).  K is
+// stored row-major with an XOR swizzle of its 16-byte chunks; V is stored
+// transposed, with keys permuted inside each 16-key group so that the P^T
+// operand can be taken from the accumulator registers as they are.
+//
+// Tiles never cross a resource boundary in encode, and the reduction order
+// depends only on local indices, so a resource's outputs are bit-identical
+// wherever it is packed and whatever its neighbours are.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace rc {
+
+namespace {
+
+constexpr int kBK = 64;        // keys per tile
+constexpr int kVTS = kBK + 8;  // V^T row stride in bf16 (144 B: conflict-free 16 B reads)
+constexpr int kThreads = 256;
+
+// Position of key k (0..63) inside the V^T row: bits 2 and 3 swapped, which is
+// the order in which the S^T accumulator hands keys to the P^T operand.
+__device__ __forceinline__ int vt_slot(int k) {
+    return (k & ~15) | (((k >> 2) & 1) << 3) | (((k >> 3) & 1) << 2) | (k & 3);
+}
+
+template <int HD>
+struct Tile {
+    static constexpr int CPR = HD / 8;              // 16-byte chunks per row
+    static constexpr int KPT = kBK * CPR / kThreads;  // keys per thread per tile (4 or 2)
+    static constexpr int NT = HD / 16;              // MFMA k-steps over head_dim
+    static constexpr int NDB = HD / 32;             // 32-wide blocks of head_dim
+    static constexpr int K_ELEMS = kBK * HD;
+    static constexpr int V_ELEMS = HD * kVTS;
+    static constexpr int STAGE = K_ELEMS + V_ELEMS;  // bf16 elements per stage
+};
+
+constexpr int kMaxSeg = 1024;
+
+template <int HD, bool ENCODE>
+struct Smem {
+    uint16_t kv[2 * Tile<HD>::STAGE];
+    int seg_start[ENCODE ? 1 : kMaxSeg + 1];
+    int seg_row[ENCODE ? 1 : kMaxSeg];
+    int scan[ENCODE ? 1 : kThreads];
+};
+
+template <int HD, bool ENCODE>
+__global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a) {
+    using TL = Tile<HD>;
+    __shared__ Smem<HD, ENCODE> sm;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, half = lane >> 5;
+
+    // block -> (q tile [longest first], unit, head quarter, group); the group
+    // is the fastest index so that one group's blocks share an XCD's L2.
+    int bid = blockIdx.x;
+    const int g = bid % a.n_kv_heads;
+    bid /= a.n_kv_heads;
+    const int hq = bid % a.n_hq;
+    bid /= a.n_hq;
+    const int unit = bid % a.n_units;
+    const int jt = a.n_qt - 1 - bid / a.n_units;
+
+    int q_len, q_row0, off, stream, pos0 = 0;
+    const uint16_t* kbase;
+    const uint16_t* vbase;
+    int n_seg = 0, s_vis = 0, ctx_row0 = 0, tc = 0;
+    if constexpr (ENCODE) {
+        const int o = a.cu_len[unit];
+        q_len = a.cu_len[unit + 1] - o;
+        q_row0 = o;
+        off = 0;
+        stream = q_len;
+        pos0 = a.pos_base ? a.pos_base[unit] : 0;
+        kbase = a.k + ((size_t)g * a.k_rows + o) * HD;
+        vbase = a.v + ((size_t)g * a.k_rows + o) * HD;
+    } else {
+        q_row0 = a.cu_q[unit];
+        q_len = a.cu_q[unit + 1] - q_row0;
+        ctx_row0 = a.cu_ctx[unit];
+        tc = a.cu_ctx[unit + 1] - ctx_row0;
+        kbase = a.k + (size_t)g * a.k_rows * HD;
+        vbase = a.v + (size_t)g * a.k_rows * HD;
+    }
+    const int wg_rows = 32 * a.rbw;
+    const int q_first = jt * wg_rows;
+    if (q_first >= q_len) return;
+    const int q_last = min(q_first + wg_rows, q_len) - 1;
+
+    if constexpr (!ENCODE) {
+        // Visible segments of this (request, layer, group): kept rows of the
+        // routed resources, request order.  Exclusive scan of their lengths.
+        const size_t e = ((size_t)unit * a.n_layers + a.layer) * a.n_kv_heads + g;
+        const int r0 = a.route_off[e];
+        n_seg = min(a.route_off[e + 1] - r0, kMaxSeg);
+        int part = 0;
+        int lens[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int s = tid * 4 + i;
+            lens[i] = 0;
+            if (s < n_seg) {
+                const int r = a.route_res[r0 + s];
+                const int k0 = a.cu_kept[r];
+                lens[i] = a.cu_kept[r + 1] - k0;
+                sm.seg_row[s] = k0;
+            }
+            part += lens[i];
+        }
+        sm.scan[tid] = part;
+        __syncthreads();
+        for (int o = 1; o < kThreads; o <<= 1) {
+            const int add = tid >= o ? sm.scan[tid - o] : 0;
+            __syncthreads();
+            sm.scan[tid] += add;
+            __syncthreads();
+        }
+        int run = sm.scan[tid] - part;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int s = tid * 4 + i;
+            if (s < n_seg) sm.seg_start[s] = run;
+            run += lens[i];
+        }
+        s_vis = sm.scan[kThreads - 1];
+        if (tid == 0) sm.seg_start[n_seg] = s_vis;
+        off = s_vis + tc - q_len;
+        stream = s_vis + tc;
+        __syncthreads();
+    }
+    const int n_tiles = (off + q_last) / kBK + 1;
+
+    const int hpw = a.hpw;
+    const int head = g * a.ratio + hq * hpw + (wave % hpw);
+    const int my_q = q_first + (wave / hpw) * 32 + l32;
+    // rows outside [0, lse_rows) of q / out are never touched
+    const int my_q_c = max(0, min(min(my_q, q_len - 1), (int)a.lse_rows - 1 - q_row0));
+    const bool store = my_q < q_len && q_row0 + my_q < a.lse_rows;
+
+    // ---- Q fragment (B operand of S^T = K Q^T): lane holds row my_q, elements
+    // d = t*16 + half*8 + [0,8) for t < NT.
+    bf16x8 qf[TL::NT];
+    {
+        const uint16_t* qrow = a.q + ((size_t)(q_row0 + my_q_c) * a.n_q_heads + head) * HD;
+        u32x4 raw[TL::NT];
+#pragma unroll
+        for (int t = 0; t < TL::NT; ++t)
+            raw[t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
+        if constexpr (ENCODE) {
+            // RoPE at the resource-local position, pairs (f, f + HD/2) are
+            // (t, t + NT/2) in this lane.
+            const int pos = pos0 + my_q_c;
+#pragma unroll
+            for (int t = 0; t < TL::NT / 2; ++t) {
+                uint32_t lo[4], hi[4];
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    float y1[2], y2[2];
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2) {
+                        const int f = t * 16 + half * 8 + w * 2 + h2;
+                        float s, c;
+                        sincos_rev_fast(rope_revolutions(pos, a.rope.rev[f]), &s, &c);
+                        const float x1 = bf16_bits_to_f32((raw[t][w] >> (16 * h2)) & 0xffffu);
+                        const float x2 =
+                            bf16_bits_to_f32((raw[t + TL::NT / 2][w] >> (16 * h2)) & 0xffffu);
+                        y1[h2] = x1 * c - x2 * s;
+                        y2[h2] = x2 * c + x1 * s;
+                    }
+                    lo[w] = pack_bf16x2(y1[0], y1[1]);
+                    hi[w] = pack_bf16x2(y2[0], y2[1]);
+                }
+                raw[t] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+                raw[t + TL::NT / 2] = u32x4{hi[0], hi[1], hi[2], hi[3]};
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < TL::NT; ++t) qf[t] = __builtin_bit_cast(bf16x8, raw[t]);
+    }
+
+    // ---- K/V tile staging.  Thread owns keys kq*KPT + [0, KPT), chunk c.
+    const int c = tid % TL::CPR;
+    const int kq = tid / TL::CPR;
+    u32x4 kreg[TL::KPT], vreg[TL::KPT];
+
+    auto row_ptr_off = [&](int p, const uint16_t*& kp, const uint16_t*& vp) {
+        p = min(p, stream - 1);
+        if constexpr (ENCODE) {
+            kp = kbase + (size_t)p * HD;
+            vp = vbase + (size_t)p * HD;
+        } else {
+            size_t row;
+            if (p < s_vis) {
+                int lo = 0, hi = n_seg - 1;  // last segment with start <= p
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (sm.seg_start[mid] <= p) lo = mid; else hi = mid - 1;
+                }
+                row = (size_t)(sm.seg_row[lo] + (p - sm.seg_start[lo]));
+                row = min(row, (size_t)a.k_rows - 1);
+                kp = kbase + row * HD;
+                vp = vbase + row * HD;
+            } else {
+                row = (size_t)ctx_row0 + (p - s_vis);
+                row = min(row, (size_t)a.c_rows - 1);
+                kp = a.ck + ((size_t)g * a.c_rows + row) * HD;
+                vp = a.cv + ((size_t)g * a.c_rows + row) * HD;
+            }
+        }
+    };
+    auto load_tile = [&](int kt) {
+#pragma unroll
+        for (int j = 0; j < TL::KPT; ++j) {
+            const uint16_t* kp;
+            const uint16_t* vp;
+            row_ptr_off(kt * kBK + kq * TL::KPT + j, kp, vp);
+            kreg[j] = *reinterpret_cast<const u32x4*>(kp + c * 8);
+            vreg[j] = *reinterpret_cast<const u32x4*>(vp + c * 8);
+        }
+    };
+    auto store_tile = [&](int buf) {
+        uint16_t* ks = sm.kv + buf * TL::STAGE;
+        uint16_t* vt = ks + TL::K_ELEMS;
+#pragma unroll
+        for (int j = 0; j < TL::KPT; ++j) {
+            const int key = kq * TL::KPT + j;
+            *reinterpret_cast<u32x4*>(ks + key * HD + ((c ^ (key % TL::CPR)) * 8)) = kreg[j];
+        }
+        const int slot = vt_slot(kq * TL::KPT);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int d = c * 8 + i;
+            const int sh = 16 * (i & 1);
+            if constexpr (TL::KPT == 4) {
+                const uint32_t w0 = ((vreg[0][i >> 1] >> sh) & 0xffffu) | (((vreg[1][i >> 1] >> sh) & 0xffffu) << 16);
+                const uint32_t w1 = ((vreg[2][i >> 1] >> sh) & 0xffffu) | (((vreg[3][i >> 1] >> sh) & 0xffffu) << 16);
+                *reinterpret_cast<uint2*>(vt + d * kVTS + slot) = make_uint2(w0, w1);
+            } else {
+                const uint32_t w0 = ((vreg[0][i >> 1] >> sh) & 0xffffu) | (((vreg[1][i >> 1] >> sh) & 0xffffu) << 16);
+                *reinterpret_cast<uint32_t*>(vt + d * kVTS + slot) = w0;
+            }
+        }
+    };
+
+    load_tile(0);
+    store_tile(0);
+    __syncthreads();
+
+    const float sl2 = a.scale_log2;
+    float m = -INFINITY;  // running max of raw logits for this lane's row
+    float lsum = 0.f;     // this lane's partial sum of exp2 weights
+    f32x16 oacc[TL::NDB];
+#pragma unroll
+    for (int db = 0; db < TL::NDB; ++db) oacc[db] = f32x16{};
+
+    const int lim = off + my_q;  // keys p <= lim are visible to this lane's row
+    for (int kt = 0; kt < n_tiles; ++kt) {
+        const int cur = kt & 1;
+        const uint16_t* ks = sm.kv + cur * TL::STAGE;
+        const uint16_t* vt = ks + TL::K_ELEMS;
+        if (kt + 1 < n_tiles) load_tile(kt + 1);
+
+        f32x16 sacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+        for (int t = 0; t < TL::NT; ++t) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const int key = kb * 32 + l32;
+                const int chunk = (t * 2 + half) ^ (key % TL::CPR);
+                const bf16x8 av = *reinterpret_cast<const bf16x8*>(ks + key * HD + chunk * 8);
+                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[t], sacc[kb], 0, 0, 0);
+            }
+        }
+        // causal / stream-end mask, only on tiles that reach past the first row's limit
+        if (kt * kBK + kBK - 1 > off + q_first) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int p = kt * kBK + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+                    if (p > lim) sacc[kb][r] = -INFINITY;
+                }
+        }
+        float mt = sacc[0][0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) mt = fmaxf(mt, sacc[0][r]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[1][r]);
+        mt = pair_max(mt);
+        const float m_new = fmaxf(m, mt);
+        if (__builtin_amdgcn_ballot_w64(m_new > m)) {
+            const float alpha = exp2f((m - m_new) * sl2);  // 0 when m == -inf
+            lsum *= alpha;
+#pragma unroll
+            for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
+            m = m_new;
+        }
+        const float msl = m * sl2;
+        bf16x8 pf[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float p[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                p[e] = exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
+                lsum += p[e];
+            }
+            u32x4 w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                       pack_bf16x2(p[6], p[7])};
+            pf[s] = __builtin_bit_cast(bf16x8, w);
+        }
+#pragma unroll
+        for (int db = 0; db < TL::NDB; ++db) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const bf16x8 av = *reinterpret_cast<const bf16x8*>(vt + (db * 32 + l32) * kVTS + s * 16 + half * 8);
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pf[s], oacc[db], 0, 0, 0);
+            }
+        }
+        if (kt + 1 < n_tiles) store_tile(cur ^ 1);
+        __syncthreads();
+    }
+
+    lsum = pair_sum(lsum);
+    if (store) {
+        const float inv = 1.0f / lsum;
+        uint16_t* orow = a.out + ((size_t)(q_row0 + my_q) * a.n_q_heads + head) * HD;
+#pragma unroll
+        for (int db = 0; db < TL::NDB; ++db)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                const int d = db * 32 + r4 * 8 + half * 4;
+                const uint2 w = make_uint2(pack_bf16x2(oacc[db][r4 * 4 + 0] * inv, oacc[db][r4 * 4 + 1] * inv),
+                                           pack_bf16x2(oacc[db][r4 * 4 + 2] * inv, oacc[db][r4 * 4 + 3] * inv));
+                *reinterpret_cast<uint2*>(orow + d) = w;
+            }
+        if (a.lse && half == 0)
+            a.lse[(size_t)head * a.lse_rows + q_row0 + my_q] =
+                m * sl2 * 0.69314718055994531f + logf(lsum);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream) {
+    const long blocks = (long)a.n_qt * a.n_units * a.n_hq * a.n_kv_heads;
+    if (blocks <= 0) return hipSuccess;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)blocks), block(kThreads);
+    if (head_dim == 128) {
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, a);
+    } else {
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace rc

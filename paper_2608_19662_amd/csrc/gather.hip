@@ -1,0 +1,142 @@
+// Index work of the method, all integer and exact:
+//   - kept-row gather (ReCache Sec. 3, "Semantic Pruning"): the retained
+//     subsequence of every resource, copied bit for bit into a compacted,
+//     head-major buffer;
+//   - route lists (Sec. 3, "Structural Pruning"): for every (request, layer,
+//     KV group), the request's resources whose route is in Omega, in request
+//     order, as a CSR with a per-entry kept-token total.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace rc {
+
+namespace {
+
+// One thread per 16-byte chunk of an output row.  The owning resource of a
+// compacted row is found by binary search over cu_kept.
+__global__ __launch_bounds__(256) void prune_gather_kernel(
+    int chunks_per_row, int n_res, const int32_t* __restrict__ cu_len,
+    const int32_t* __restrict__ cu_kept, const int32_t* __restrict__ kept_idx, long total_T,
+    long total_kept, long total_chunks, const u32x4* __restrict__ kc, const u32x4* __restrict__ vc,
+    u32x4* __restrict__ ko, u32x4* __restrict__ vo) {
+    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total_chunks) return;
+    const int c = (int)(idx % chunks_per_row);
+    const long row = idx / chunks_per_row;
+    const long g = row / total_kept;
+    const int j = (int)(row % total_kept);
+    int lo = 0, hi = n_res - 1;  // last r with cu_kept[r] <= j
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (cu_kept[mid] <= j) lo = mid; else hi = mid - 1;
+    }
+    long src = (long)cu_len[lo] + kept_idx[j];
+    src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
+    const size_t s = ((size_t)g * total_T + src) * chunks_per_row + c;
+    ko[idx] = kc[s];
+    vo[idx] = vc[s];
+}
+
+// Entry e = (b * L + l) * G + g: count the visible resources and their kept rows.
+__global__ __launch_bounds__(256) void route_count_kernel(
+    int n_req, int L, int G, int n_res, const int32_t* __restrict__ req_res_off,
+    const int32_t* __restrict__ req_res, const uint8_t* __restrict__ mask,
+    const int32_t* __restrict__ cu_kept, int32_t* __restrict__ route_off,
+    int32_t* __restrict__ route_tokens) {
+    const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= (long)n_req * L * G) return;
+    const int g = (int)(e % G);
+    const int l = (int)((e / G) % L);
+    const int b = (int)(e / ((long)G * L));
+    int cnt = 0, tok = 0;
+    for (int j = req_res_off[b]; j < req_res_off[b + 1]; ++j) {
+        const int r = req_res[j];
+        if (r < 0 || r >= n_res) continue;
+        if (mask[((size_t)r * L + l) * G + g]) {
+            ++cnt;
+            tok += cu_kept[r + 1] - cu_kept[r];
+        }
+    }
+    route_off[e + 1] = cnt;
+    route_tokens[e] = tok;
+}
+
+// In-place inclusive scan of route_off[1..E] by one block; route_off[0] = 0.
+__global__ __launch_bounds__(1024) void route_scan_kernel(long E, int32_t* __restrict__ route_off) {
+    __shared__ int part[1024];
+    const int tid = threadIdx.x;
+    const long per = (E + 1023) / 1024;
+    const long a = 1 + tid * per, b = a + per < E + 1 ? a + per : E + 1;
+    int s = 0;
+    for (long i = a; i < b; ++i) s += route_off[i];
+    part[tid] = s;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+        const int add = tid >= o ? part[tid - o] : 0;
+        __syncthreads();
+        part[tid] += add;
+        __syncthreads();
+    }
+    int run = part[tid] - s;
+    for (long i = a; i < b; ++i) {
+        run += route_off[i];
+        route_off[i] = run;
+    }
+    if (tid == 0) route_off[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void route_fill_kernel(
+    int n_req, int L, int G, int n_res, const int32_t* __restrict__ req_res_off,
+    const int32_t* __restrict__ req_res, const uint8_t* __restrict__ mask,
+    const int32_t* __restrict__ route_off, int32_t* __restrict__ route_res) {
+    const long e = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= (long)n_req * L * G) return;
+    const int g = (int)(e % G);
+    const int l = (int)((e / G) % L);
+    const int b = (int)(e / ((long)G * L));
+    int w = route_off[e];
+    for (int j = req_res_off[b]; j < req_res_off[b + 1]; ++j) {
+        const int r = req_res[j];
+        if (r < 0 || r >= n_res) continue;
+        if (mask[((size_t)r * L + l) * G + g]) route_res[w++] = r;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
+                               const int32_t* cu_kept, const int32_t* kept_idx, long total_T,
+                               long total_kept, int n_kv_heads, int head_dim, const void* k_cache,
+                               const void* v_cache, void* k_kept, void* v_kept, hipStream_t s) {
+    const int cpr = head_dim * elem_bytes / 16;
+    const long total = (long)n_kv_heads * total_kept * cpr;
+    if (total == 0) return hipSuccess;
+    const long blocks = (total + 255) / 256;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(prune_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr, n_res,
+                       cu_len, cu_kept, kept_idx, total_T, total_kept, total,
+                       static_cast<const u32x4*>(k_cache), static_cast<const u32x4*>(v_cache),
+                       static_cast<u32x4*>(k_kept), static_cast<u32x4*>(v_kept));
+    return hipGetLastError();
+}
+
+hipError_t launch_build_routes(int n_req, const int32_t* req_res_off, const int32_t* req_res,
+                               int n_res, int n_layers, int n_kv_heads, const uint8_t* mask,
+                               const int32_t* cu_kept, int32_t* route_off, int32_t* route_res,
+                               int32_t* route_tokens, hipStream_t s) {
+    const long E = (long)n_req * n_layers * n_kv_heads;
+    const unsigned blocks = (unsigned)((E + 255) / 256);
+    hipLaunchKernelGGL(route_count_kernel, dim3(blocks), dim3(256), 0, s, n_req, n_layers,
+                       n_kv_heads, n_res, req_res_off, req_res, mask, cu_kept, route_off,
+                       route_tokens);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(route_scan_kernel, dim3(1), dim3(1024), 0, s, E, route_off);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(route_fill_kernel, dim3(blocks), dim3(256), 0, s, n_req, n_layers,
+                       n_kv_heads, n_res, req_res_off, req_res, mask, route_off, route_res);
+    return hipGetLastError();
+}
+
+}  // namespace rc

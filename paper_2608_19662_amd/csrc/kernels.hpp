@@ -1,0 +1,131 @@
+// Argument blocks and launchers of the gfx950 kernels.  The C-ABI layer
+// (api.hip) validates every scalar before it fills these and launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace rc {
+
+// bf16 MFMA flash attention (encode or conversation prefill).
+struct AttnArgs {
+    // decomposition: blocks = n_qt * n_units * n_hq * n_kv_heads
+    int n_q_heads, n_kv_heads, ratio;
+    int hpw;      // query heads per block (min(ratio, 4))
+    int rbw;      // 32-row blocks per block (4 / hpw)
+    int n_hq;     // blocks per group along heads (ratio / hpw)
+    int n_units;  // resources (encode) or requests (prefill)
+    int n_qt;     // query tiles per unit (ceil(max rows / (32 * rbw)))
+    float scale_log2;  // softmax_scale * log2(e)
+    const uint16_t* q;
+    uint16_t* out;
+    float* lse;
+    long lse_rows;      // rows of q / out / lse (total_T or total_q); bounds every row index
+    const uint16_t* k;  // encode: rotated K cache; prefill: kept resource rows
+    const uint16_t* v;
+    long k_rows;        // rows per KV head in k / v
+    // encode
+    const int32_t* cu_len;
+    const int32_t* pos_base;
+    RopeRev rope;
+    // prefill
+    const int32_t* cu_q;
+    const int32_t* cu_ctx;
+    const uint16_t* ck;
+    const uint16_t* cv;
+    long c_rows;
+    int layer, n_layers;
+    const int32_t* route_off;
+    const int32_t* route_res;
+    const int32_t* cu_kept;
+};
+hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream);
+
+// fp32 reference-precision attention (encode or conversation attend).
+struct AttnF32Args {
+    int n_q_heads, n_kv_heads, ratio, head_dim;
+    int n_units, max_rows;  // grid: max_rows x n_units x n_q_heads waves
+    float scale;
+    const float* q;
+    float* out;
+    float* lse;
+    long lse_rows;
+    const float* k;
+    const float* v;
+    long k_rows;
+    const int32_t* cu_len;
+    const int32_t* pos_base;
+    RopeRev rope;
+    const int32_t* cu_q;
+    const int32_t* cu_ctx;
+    const float* ck;
+    const float* cv;
+    long c_rows;
+    int layer, n_layers;
+    const int32_t* route_off;
+    const int32_t* route_res;
+    const int32_t* cu_kept;
+};
+hipError_t launch_attn_f32(const AttnF32Args& a, bool encode, hipStream_t stream);
+
+// RoPE + cache write / in-place RoPE.
+struct RopeArgs {
+    int T, n_heads, head_dim, dtype;  // dtype: 0 f32, 1 bf16
+    const int32_t* pos;               // explicit positions [T], or NULL with cu_len
+    const int32_t* cu_len;            // resource-local positions from packing offsets
+    const int32_t* pos_base;
+    int n_res;
+    RopeRev rope;
+    const void* x;  // source [T][H][d]
+    void* y;        // rotated destination: in place ([T][H][d]) or cache ([H][rows][d])
+    const void* v;  // optional value copy source [T][H][d]
+    void* v_dst;    // value cache [H][rows][d]
+    long cache_rows;
+    int row0;
+    int to_cache;  // 1: write head-major caches at row0 + t
+};
+hipError_t launch_rope(const RopeArgs& a, hipStream_t stream);
+
+// Kept-row gather.
+hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
+                               const int32_t* cu_kept, const int32_t* kept_idx, long total_T,
+                               long total_kept, int n_kv_heads, int head_dim, const void* k_cache,
+                               const void* v_cache, void* k_kept, void* v_kept, hipStream_t s);
+
+// Route CSR build.
+hipError_t launch_build_routes(int n_req, const int32_t* req_res_off, const int32_t* req_res,
+                               int n_res, int n_layers, int n_kv_heads, const uint8_t* mask,
+                               const int32_t* cu_kept, int32_t* route_off, int32_t* route_res,
+                               int32_t* route_tokens, hipStream_t s);
+
+// Split-KV decode (one query per request) and its LSE merge.
+struct DecodeArgs {
+    int n_req, n_q_heads, n_kv_heads, ratio, head_dim, n_splits;
+    float scale_log2;
+    const uint16_t* q;
+    uint16_t* out;
+    float* lse;
+    long lse_rows;
+    const uint16_t* rk;
+    const uint16_t* rv;
+    long r_rows;
+    const uint16_t* ck;
+    const uint16_t* cv;
+    long c_rows;
+    const int32_t* cu_q;
+    const int32_t* cu_ctx;
+    int layer, n_layers;
+    const int32_t* route_off;
+    const int32_t* route_res;
+    const int32_t* cu_kept;
+    float* ws_o;   // [n_req][Hq][n_splits][head_dim]
+    float* ws_ml;  // [n_req][Hq][n_splits][2]  (max in log2 units, sum)
+};
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+size_t decode_workspace_bytes(int n_req, int n_q_heads, int head_dim, int n_splits);
+int decode_splits(int n_req, int n_kv_heads, int max_kv);
+
+}  // namespace rc

@@ -1,0 +1,241 @@
+"""Thin Python binding of librecache.so (the C ABI in include/recache.h).
+
+Argument marshalling only: every function takes torch CUDA tensors, checks
+that they are contiguous device tensors of the expected dtype (passing a host
+pointer to a kernel would fault the GPU), reads sizes from their shapes and
+calls the C entry point of the same name on the current HIP stream.  All
+arithmetic happens in the library's HIP kernels; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librecache.so")
+
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+
+_lib = None
+
+_c_int, _c_dbl, _c_flt, _c_p, _c_size = (ctypes.c_int, ctypes.c_double, ctypes.c_float,
+                                         ctypes.c_void_p, ctypes.c_size_t)
+
+_SIGS = {
+    "recache_version": ([], _c_int),
+    "recache_last_error": ([], ctypes.c_char_p),
+    "recache_rope_q": ([_c_int, _c_int, _c_int, _c_int, _c_dbl, _c_p, _c_p, _c_p], _c_int),
+    "recache_rope_kv": ([_c_int, _c_int, _c_int, _c_int, _c_dbl, _c_p, _c_p, _c_p, _c_p, _c_p,
+                         _c_int, _c_int, _c_p], _c_int),
+    "recache_encode_resources": ([_c_int, _c_int, _c_p, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                  _c_dbl, _c_p, _c_flt, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                  _c_p], _c_int),
+    "recache_encode_attention": ([_c_int, _c_int, _c_p, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                  _c_dbl, _c_p, _c_flt, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p],
+                                 _c_int),
+    "recache_prune_gather": ([_c_int, _c_int, _c_p, _c_p, _c_p, _c_int, _c_int, _c_int, _c_int,
+                              _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
+    "recache_build_routes": ([_c_int, _c_p, _c_p, _c_int, _c_int, _c_int, _c_int, _c_p, _c_p,
+                              _c_p, _c_p, _c_p, _c_p], _c_int),
+    "recache_attend_workspace_bytes": ([_c_int] * 7, _c_size),
+    "recache_attend_cached": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_int,
+                               _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p, _c_p, _c_p,
+                               _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                               _c_p, _c_size, _c_p], _c_int),
+    "recache_check_offsets": ([_c_p, _c_int, _c_int, _c_int], _c_int),
+    "recache_check_kept": ([_c_p, _c_p, _c_p, _c_int], _c_int),
+}
+
+EXPORTS = tuple(_SIGS)
+
+
+class RecacheError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s (status %d)" % (msg, code))
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """Load librecache.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("librecache.so is not built; run `python -m paper_2608_19662_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().recache_last_error().decode()
+
+
+def version() -> int:
+    return lib().recache_version()
+
+
+def _call(name, *args):
+    rc = getattr(lib(), name)(*args)
+    if rc != OK:
+        raise RecacheError(rc, "%s: %s" % (name, last_error()))
+    return rc
+
+
+# ------------------------------------------------------------- marshalling
+
+def _dev(t, name, dtypes=None):
+    """Device pointer of a contiguous CUDA tensor (None -> NULL)."""
+    if t is None:
+        return None
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError("%s has dtype %s, expected one of %s" % (name, t.dtype, dtypes))
+    return t.data_ptr()
+
+
+def _dtype_code(t):
+    import torch
+
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError("floating tensors must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _i32():
+    import torch
+
+    return (torch.int32,)
+
+
+def _same(ref, *ts):
+    for t in ts:
+        if t is not None and t.dtype != ref.dtype:
+            raise TypeError("all floating tensors of a call share one dtype")
+
+
+# ------------------------------------------------------------- entry points
+
+def rope_q(x, pos, rope_base: float, stream=None):
+    """In-place RoPE of x[T][H][d] at positions pos[T]."""
+    T, H, d = x.shape
+    _call("recache_rope_q", _dtype_code(x), T, H, d, rope_base, _dev(pos, "pos", _i32()),
+          _dev(x, "x"), _stream(stream))
+
+
+def rope_kv(k, v, pos, rope_base: float, k_cache, v_cache, row0: int = 0, stream=None):
+    """Rotated k and plain v into head-major caches [Hkv][rows][d] at row0."""
+    T, Hkv, d = k.shape
+    _same(k, v, k_cache, v_cache)
+    _call("recache_rope_kv", _dtype_code(k), T, Hkv, d, rope_base, _dev(pos, "pos", _i32()),
+          _dev(k, "k"), _dev(v, "v"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+          k_cache.shape[1], row0, _stream(stream))
+
+
+def encode_resources(q, k, v, cu_len, max_len: int, rope_base: float, out, k_cache, v_cache,
+                     lse=None, pos_base=None, softmax_scale: float = 0.0, stream=None):
+    """One layer of block-diagonal resource encoding (see recache.h)."""
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    _same(q, k, v, out, k_cache, v_cache)
+    _call("recache_encode_resources", _dtype_code(q), cu_len.numel() - 1,
+          _dev(cu_len, "cu_len", _i32()), T, int(max_len), Hq, Hkv, d, rope_base,
+          _dev(pos_base, "pos_base", _i32()), softmax_scale, _dev(q, "q"), _dev(k, "k"),
+          _dev(v, "v"), _dev(out, "out"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+          _dev(lse, "lse"), _stream(stream))
+
+
+def encode_attention(q, k_cache, v_cache, cu_len, max_len: int, rope_base: float, out, lse=None,
+                     pos_base=None, softmax_scale: float = 0.0, stream=None):
+    """Attention half of the encode over already built caches [Hkv][T][d]."""
+    T, Hq, d = q.shape
+    Hkv = k_cache.shape[0]
+    _same(q, k_cache, v_cache, out)
+    _call("recache_encode_attention", _dtype_code(q), cu_len.numel() - 1,
+          _dev(cu_len, "cu_len", _i32()), T, int(max_len), Hq, Hkv, d, rope_base,
+          _dev(pos_base, "pos_base", _i32()), softmax_scale, _dev(q, "q"),
+          _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(out, "out"), _dev(lse, "lse"),
+          _stream(stream))
+
+
+def prune_gather(k_cache, v_cache, cu_len, cu_kept, kept_idx, k_kept, v_kept, stream=None):
+    """Kept-row compaction of one layer's head-major caches."""
+    Hkv, T, d = k_cache.shape
+    _same(k_cache, v_cache, k_kept, v_kept)
+    _call("recache_prune_gather", _dtype_code(k_cache), cu_len.numel() - 1,
+          _dev(cu_len, "cu_len", _i32()), _dev(cu_kept, "cu_kept", _i32()),
+          _dev(kept_idx, "kept_idx", _i32()), T, k_kept.shape[1], Hkv, d,
+          _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(k_kept, "k_kept"),
+          _dev(v_kept, "v_kept"), _stream(stream))
+
+
+def build_routes(req_res_off, req_res, route_mask, cu_kept, route_off, route_res, route_tokens,
+                 stream=None):
+    """Route CSR for every (request, layer, KV group); route_mask is [n_res][L][G] uint8."""
+    import torch
+
+    n_res, L, G = route_mask.shape
+    _call("recache_build_routes", req_res_off.numel() - 1, _dev(req_res_off, "req_res_off", _i32()),
+          _dev(req_res, "req_res", _i32()), req_res.numel(), n_res, L, G,
+          _dev(route_mask, "route_mask", (torch.uint8,)), _dev(cu_kept, "cu_kept", _i32()),
+          _dev(route_off, "route_off", _i32()), _dev(route_res, "route_res", _i32()),
+          _dev(route_tokens, "route_tokens", _i32()), _stream(stream))
+
+
+def attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads, n_kv_heads, head_dim) -> int:
+    return int(lib().recache_attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads,
+                                                    n_kv_heads, head_dim))
+
+
+def attend_cached(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k, res_v, cu_kept,
+                  route_off, route_res, route_tokens, layer: int, n_layers: int, out, lse=None,
+                  workspace=None, max_kv: int = 0, max_route_len: int = 1024,
+                  softmax_scale: float = 0.0, stream=None):
+    """Conversation queries over routed kept resource rows + causal context (one layer)."""
+    total_q, Hq, d = q.shape
+    Hkv = ctx_k.shape[0]
+    _same(q, ctx_k, ctx_v, res_k, res_v, out)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _call("recache_attend_cached", _dtype_code(q), layer, n_layers, cu_q.numel() - 1,
+          _dev(cu_q, "cu_q", _i32()), _dev(cu_ctx, "cu_ctx", _i32()), total_q, int(max_q),
+          int(max_ctx), int(max_kv), int(max_route_len), Hq, Hkv, d, softmax_scale, _dev(q, "q"),
+          _dev(ctx_k, "ctx_k"), _dev(ctx_v, "ctx_v"), ctx_k.shape[1], _dev(res_k, "res_k"),
+          _dev(res_v, "res_v"), res_k.shape[1], _dev(cu_kept, "cu_kept", _i32()),
+          _dev(route_off, "route_off", _i32()), _dev(route_res, "route_res", _i32()),
+          _dev(route_tokens, "route_tokens", _i32()), _dev(out, "out"), _dev(lse, "lse"),
+          _dev(workspace, "workspace"), ws_bytes, _stream(stream))
+
+
+def check_offsets(cu, total: int, strict: bool = True) -> None:
+    """Host validator of packing offsets (numpy / list)."""
+    a = np.ascontiguousarray(np.asarray(cu, dtype=np.int32))
+    _call("recache_check_offsets", a.ctypes.data, len(a) - 1, int(total), int(strict))
+
+
+def check_kept(cu_len, cu_kept, kept_idx) -> None:
+    """Host validator of kept-token lists (numpy / list)."""
+    a = np.ascontiguousarray(np.asarray(cu_len, dtype=np.int32))
+    b = np.ascontiguousarray(np.asarray(cu_kept, dtype=np.int32))
+    c = np.ascontiguousarray(np.asarray(kept_idx, dtype=np.int32))
+    _call("recache_check_kept", a.ctypes.data, b.ctypes.data, c.ctypes.data, len(a) - 1)

@@ -1,0 +1,94 @@
+"""Helpers for the GPU parity tests: device copies of workload structure,
+the route build, and the tolerance rules.
+
+Tolerances (stated once, used by every GPU test):
+  fp32 inputs:  |gpu - oracle| <= 1e-5 everywhere.
+  bf16 inputs:  |gpu - oracle| <= 1e-2 + 2^-9 |oracle| everywhere: the 1e-2
+                bound for fp32 accumulation over bf16 inputs, widened by the
+                half-ulp of rounding the output to bf16 (a correctly rounded
+                bf16 value of magnitude in [4, 8) can be 2^-6 away).
+  index work:   bit-exact.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2608_19662_amd import recache as rc
+
+DEV = "cuda"
+
+
+def i32(a):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.int32))).to(DEV)
+
+
+def f64(t) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def check(gpu, ref, dtype: str, name: str):
+    """Assert the tolerance rule; returns the max abs error."""
+    g = f64(gpu)
+    ref = np.asarray(ref, np.float64)
+    assert g.shape == ref.shape, (name, g.shape, ref.shape)
+    err = np.abs(g - ref)
+    if dtype == "f32":
+        bound = np.full_like(ref, 1e-5)
+    else:
+        bound = 1e-2 + 2.0 ** -9 * np.abs(ref)
+    bad = ~(err <= bound)
+    assert not bad.any(), "%s: %d of %d out of tolerance, max abs err %.3g at %s" % (
+        name, int(bad.sum()), bad.size, float(np.nanmax(err)), np.argwhere(bad)[0].tolist())
+    return float(err.max()) if err.size else 0.0
+
+
+class Routes:
+    """Device structure of an AttendWorkload plus its route CSR (GPU-built)."""
+
+    def __init__(self, w, stream=None):
+        self.w = w
+        self.cu_q = i32(w.cu_q)
+        self.cu_ctx = i32(w.cu_ctx)
+        self.cu_rows = i32(w.cu_rows)
+        self.req_res_off = i32(w.req_res_off)
+        self.req_res = i32(w.req_res if len(w.req_res) else [0])
+        self.mask = torch.from_numpy(np.ascontiguousarray(w.mask.astype(np.uint8))).to(DEV)
+        E = w.n_req * w.n_layers * w.n_kv_heads
+        self.route_off = torch.empty(E + 1, dtype=torch.int32, device=DEV)
+        cap = max(1, int(w.req_res_off[-1]) * w.n_layers * w.n_kv_heads)
+        self.route_res = torch.empty(cap, dtype=torch.int32, device=DEV)
+        self.route_tokens = torch.empty(E, dtype=torch.int32, device=DEV)
+        if len(w.req_res) == 0:
+            # no resource anywhere: every route list is empty
+            self.route_off.zero_()
+            self.route_tokens.zero_()
+        else:
+            rc.build_routes(self.req_res_off, self.req_res, self.mask, self.cu_rows, self.route_off,
+                            self.route_res, self.route_tokens, stream=stream)
+        per_req = np.diff(w.req_res_off)
+        self.max_route_len = int(per_req.max()) if len(per_req) else 0
+        self.max_q = int(np.max(w.q_lens))
+        self.max_ctx = int(np.max(w.ctx_lens))
+
+    def max_kv(self, layer=None):
+        tok = self.route_tokens.cpu().numpy().reshape(self.w.n_req, self.w.n_layers, -1)
+        if layer is not None:
+            tok = tok[:, layer]
+        return int((tok.reshape(self.w.n_req, -1).max(1) + self.w.ctx_lens).max())
+
+    def workspace(self, max_kv):
+        w = self.w
+        n = rc.attend_workspace_bytes(w.n_req, self.max_q, self.max_ctx, max_kv, w.n_q_heads,
+                                      w.n_kv_heads, w.head_dim)
+        return torch.empty(max(n, 4) // 4, dtype=torch.float32, device=DEV) if n else None
+
+    def attend(self, q, ck, cv, rk, rv, layer, lse=True, workspace=None, max_kv=0, stream=None):
+        w = self.w
+        out = torch.empty_like(q)
+        l = torch.empty(w.n_q_heads, q.shape[0], dtype=torch.float32, device=DEV) if lse else None
+        rc.attend_cached(q, ck, cv, self.cu_q, self.cu_ctx, self.max_q, self.max_ctx, rk, rv,
+                         self.cu_rows, self.route_off, self.route_res, self.route_tokens, layer,
+                         w.n_layers, out, lse=l, workspace=workspace, max_kv=max_kv,
+                         max_route_len=max(self.max_route_len, 1), stream=stream)
+        return out, l

@@ -1,0 +1,144 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+symbol declared in include/recache.h, and rejects bad arguments on the host
+with the documented status before any HIP call (so fake, non-null device
+pointers below are never dereferenced)."""
+import os
+import re
+
+import pytest
+
+from paper_2608_19662_amd import recache as rc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "recache.h")
+FAKE = 0x1000  # never reaches a kernel: every call below fails validation
+
+
+def declared_symbols():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(recache_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = rc.lib()
+    names = declared_symbols()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(rc.EXPORTS) == names
+
+
+def test_version_and_clean_error():
+    assert rc.version() == 100
+    rc.check_offsets([0, 3, 5], 5)
+    assert rc.last_error() == ""
+
+
+def test_check_offsets():
+    rc.check_offsets([0, 1, 1, 4], 4, strict=False)
+    for bad, total, strict in [([1, 2], 2, True), ([0, 2, 1], 1, False), ([0, 2, 2], 2, True),
+                               ([0, 2, 3], 4, True)]:
+        with pytest.raises(rc.RecacheError) as e:
+            rc.check_offsets(bad, total, strict)
+        assert e.value.code == rc.EINVAL
+        assert rc.last_error()
+
+
+def test_check_kept():
+    rc.check_kept([0, 3, 5], [0, 2, 3], [0, 2, 1])
+    for cu_kept, kept in [([0, 2, 3], [2, 0, 1]), ([0, 2, 3], [0, 3, 1]), ([0, 0, 1], [1]),
+                          ([0, 2, 3], [1, 1, 0]), ([0, 4, 5], [0, 1, 2, 2, 0])]:
+        with pytest.raises(rc.RecacheError) as e:
+            rc.check_kept([0, 3, 5], cu_kept, kept)
+        assert e.value.code == rc.EINVAL
+
+
+def enc(**kw):
+    a = dict(dtype=1, n_res=2, cu_len=FAKE, total_T=10, max_len=6, Hq=32, Hkv=8, d=128,
+             base=1e6, pos_base=None, scale=0.0, q=FAKE, k=FAKE, v=FAKE, out=FAKE, kc=FAKE,
+             vc=FAKE, lse=None, stream=None)
+    a.update(kw)
+    return rc.lib().recache_encode_resources(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=96), rc.EUNSUPPORTED),
+    (dict(dtype=2), rc.EUNSUPPORTED),
+    (dict(Hq=30), rc.EINVAL),
+    (dict(Hq=24), rc.EUNSUPPORTED),  # 3 query heads per KV head on the bf16 kernels
+    (dict(n_res=0), rc.EINVAL),
+    (dict(total_T=1), rc.EINVAL),
+    (dict(max_len=0), rc.EINVAL),
+    (dict(max_len=11), rc.EINVAL),
+    (dict(q=None), rc.EINVAL),
+    (dict(cu_len=None), rc.EINVAL),
+    (dict(base=0.5), rc.EINVAL),
+    (dict(scale=float("nan")), rc.EINVAL),
+])
+def test_encode_rejects(kw, code):
+    assert enc(**kw) == code
+    assert rc.last_error()
+
+
+def test_encode_fp32_any_ratio_passes_head_check():
+    # fp32 path accepts 3 query heads per KV head; the next check (null q) still fires
+    assert enc(dtype=0, Hq=24, q=None) == rc.EINVAL
+    assert "null" in rc.last_error()
+
+
+def att(**kw):
+    a = dict(dtype=1, layer=0, n_layers=36, n_req=2, cu_q=FAKE, cu_ctx=FAKE, total_q=2, max_q=1,
+             max_ctx=16, max_kv=0, max_route_len=32, Hq=32, Hkv=8, d=128, scale=0.0, q=FAKE,
+             ck=FAKE, cv=FAKE, ctx_rows=32, rk=FAKE, rv=FAKE, res_rows=8, cu_kept=FAKE,
+             route_off=FAKE, route_res=FAKE, route_tokens=FAKE, out=FAKE, lse=None,
+             ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return rc.lib().recache_attend_cached(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(layer=36), rc.EINVAL),
+    (dict(layer=-1), rc.EINVAL),
+    (dict(max_q=17), rc.EINVAL),          # Tq > Tc
+    (dict(max_q=0), rc.EINVAL),
+    (dict(total_q=1), rc.EINVAL),
+    (dict(max_route_len=2000), rc.EUNSUPPORTED),
+    (dict(d=80), rc.EUNSUPPORTED),
+    (dict(res_rows=0), rc.EINVAL),
+    (dict(route_res=None), rc.EINVAL),
+    (dict(ws=None), rc.EWORKSPACE),       # decode needs split-KV scratch
+    (dict(ws=FAKE, ws_bytes=16), rc.EWORKSPACE),
+])
+def test_attend_rejects(kw, code):
+    assert att(**kw) == code
+    assert rc.last_error()
+
+
+def test_workspace_sizes():
+    n = rc.attend_workspace_bytes(64, 1, 4096, 9000, 32, 8, 128)
+    assert n > 0 and n % 4 == 0
+    assert rc.attend_workspace_bytes(8, 2048, 2048, 0, 32, 8, 128) == 0
+
+
+def test_prune_and_routes_reject():
+    L = rc.lib()
+    assert L.recache_prune_gather(1, 2, FAKE, FAKE, FAKE, 10, 11, 8, 128, FAKE, FAKE, FAKE, FAKE,
+                                  None) == rc.EINVAL
+    assert L.recache_prune_gather(1, 2, FAKE, FAKE, FAKE, 10, 1, 8, 128, FAKE, FAKE, FAKE, FAKE,
+                                  None) == rc.EINVAL
+    assert L.recache_prune_gather(1, 2, FAKE, FAKE, None, 10, 4, 8, 128, FAKE, FAKE, FAKE, FAKE,
+                                  None) == rc.EINVAL
+    assert L.recache_build_routes(0, FAKE, FAKE, 4, 4, 36, 8, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                  None) == rc.EINVAL
+    assert L.recache_build_routes(2, FAKE, FAKE, 2 ** 28, 4, 36, 8, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                  None) == rc.EINVAL
+    assert L.recache_rope_kv(1, 8, 8, 128, 1e4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 4,
+                             None) == rc.EINVAL  # rows [4, 12) overflow 10
+
+
+def test_python_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(4, 2, 64)
+    with pytest.raises(TypeError):
+        rc.rope_q(x, torch.zeros(4, dtype=torch.int32), 1e4)

@@ -1,0 +1,398 @@
+"""GPU parity: every hot-path step through the C ABI against the fp64 oracle.
+
+Small cases span several tiles and ragged tails; the full-size workloads run
+in the launch configuration the benchmark times and are checked on sampled
+outputs (whole resources for encode, sampled query rows for prefill, every
+row of sampled layers for decode).  Tolerances are in gpu_helpers.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import DEV, Routes, check, f64, i32
+from paper_2608_19662_amd import recache as rc
+from paper_2608_19662_amd.workloads import (AttendWorkload, EncodeWorkload, config, draw_kept,
+                                            draw_lengths, normal, prefix)
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_encode(w: EncodeWorkload, q, k, v, pos_base=None):
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    out = torch.empty_like(q)
+    kc = torch.empty(Hkv, T, d, dtype=q.dtype, device=DEV)
+    vc = torch.empty_like(kc)
+    lse = torch.empty(Hq, T, dtype=torch.float32, device=DEV)
+    rc.encode_resources(q, k, v, i32(w.cu_len), int(w.lengths.max()), w.rope_base, out, kc, vc,
+                        lse=lse, pos_base=None if pos_base is None else i32(pos_base))
+    torch.cuda.synchronize()
+    return out, kc, vc, lse
+
+
+def print_case(*a):
+    print("case:", *a, flush=True)
+
+
+# ---------------------------------------------------------------- config 1 (fp32)
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_config1_end_to_end(dtype):
+    """Tiny layer: encode four resources at local positions, then 48 context
+    tokens (positions 312 + j) over Bernoulli(0.5) routes, no pruning."""
+    print_case("config1", dtype)
+    c = config(1)
+    w, a = c["encode"], c["attend"]
+    w.dtype = a.dtype = dtype
+    q, k, v = w.tensors("cpu")
+    out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
+    check(out, ref["out"], dtype, "encode out")
+    check(kc, ref["k_cache"], dtype, "k_cache")
+    assert torch.equal(vc.cpu(), v.permute(1, 0, 2).contiguous())
+    check(lse, ref["lse"], "f32" if dtype == "f32" else "bf16", "encode lse")
+
+    Tc, Hq, Hkv, d = 48, 8, 2, 64
+    dt = q.dtype
+    cq = normal((Tc, Hq, d), dt, 1, 7)
+    ckr = normal((Tc, Hkv, d), dt, 1, 8)
+    cvr = normal((Tc, Hkv, d), dt, 1, 9)
+    pos = np.arange(Tc, dtype=np.int32) + a.extra["ctx_pos0"]
+    gq = cq.to(DEV)
+    rc.rope_q(gq, i32(pos), 1e4)
+    gck = torch.empty(Hkv, Tc, d, dtype=dt, device=DEV)
+    gcv = torch.empty_like(gck)
+    rc.rope_kv(ckr.to(DEV), cvr.to(DEV), i32(pos), 1e4, gck, gcv)
+    rt = Routes(a)
+    gout, glse = rt.attend(gq, gck, gcv, kc, vc, 0)
+    torch.cuda.synchronize()
+    rq = oracle.rope(cq, pos, 1e4)
+    rk = oracle.rope(ckr, pos, 1e4)
+    check(gq, rq, dtype, "rope_q")
+    check(gck, rk.transpose(1, 0, 2), dtype, "rope_kv")
+    rout, rlse = oracle.attend(rq, np.ascontiguousarray(rk.transpose(1, 0, 2)),
+                               oracle.host_view(cvr).transpose(1, 0, 2).astype(np.float64).copy(),
+                               a.cu_q, a.cu_ctx, ref["k_cache"], ref["v_cache"], a.cu_len,
+                               a.req_res_off, a.req_res, a.mask, 0)
+    check(gout, rout, dtype, "attend out")
+    check(glse, rlse.T, dtype, "attend lse")
+
+
+# ---------------------------------------------------------------- encode, bf16 MFMA
+
+ENC_LENGTHS = [1, 2, 31, 32, 33, 63, 64, 65, 97, 128, 129, 200]
+
+
+@pytest.mark.parametrize("Hq,Hkv,d", [(32, 8, 128), (8, 2, 64), (8, 8, 128), (16, 8, 128),
+                                      (64, 8, 128), (16, 2, 64)])
+def test_encode_bf16_ragged(Hq, Hkv, d):
+    print_case("encode ragged", Hq, Hkv, d)
+    w = EncodeWorkload(seed=11, lengths=np.array(ENC_LENGTHS, np.int32), n_q_heads=Hq,
+                       n_kv_heads=Hkv, head_dim=d, dtype="bf16", rope_base=1e6)
+    q, k, v = w.tensors("cpu")
+    out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
+    check(out, ref["out"], "bf16", "out")
+    check(kc, ref["k_cache"], "bf16", "k_cache")
+    check(lse, ref["lse"], "bf16", "lse")
+    # first token of every resource sees only itself: its output is its V row exactly
+    vv = v.to(DEV)
+    for r in range(len(ENC_LENGTHS)):
+        o = int(w.cu_len[r])
+        for h in range(Hq):
+            assert torch.equal(out[o, h], vv[o, h // (Hq // Hkv)])
+
+
+def test_encode_pos_base_shift():
+    """Explicit per-resource position bases (global 'Block' positions): the
+    cache changes, the attention output does not (relative positions)."""
+    print_case("encode pos_base")
+    w = EncodeWorkload(seed=12, lengths=np.array([40, 70, 130], np.int32), n_q_heads=32,
+                       n_kv_heads=8, head_dim=128, dtype="bf16", rope_base=1e6)
+    q, k, v = w.tensors("cpu")
+    pb = np.array([0, 40, 110], np.int32)
+    out, kc, _, _ = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV), pos_base=pb)
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base, pos_base=pb)
+    check(out, ref["out"], "bf16", "out")
+    check(kc, ref["k_cache"], "bf16", "k_cache")
+
+
+def test_encode_composition_invariance_bitexact():
+    """A resource's outputs and cache rows are bit-identical whatever its
+    packing offset and neighbours."""
+    print_case("encode invariance")
+    lengths = np.array([300, 77, 513, 64, 129], np.int32)
+    w = EncodeWorkload(seed=13, lengths=lengths, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                       dtype="bf16", rope_base=1e6)
+    q, k, v = (t.to(DEV) for t in w.tensors("cpu"))
+    out, kc, vc, lse = gpu_encode(w, q, k, v)
+    cu = w.cu_len
+    perm = [3, 0, 4, 2, 1]
+    sl = lambda t, r: t[cu[r]:cu[r + 1]]
+    w2 = EncodeWorkload(seed=13, lengths=lengths[perm], n_q_heads=32, n_kv_heads=8, head_dim=128,
+                        dtype="bf16", rope_base=1e6)
+    cat = lambda t: torch.cat([sl(t, r) for r in perm]).contiguous()
+    out2, kc2, vc2, lse2 = gpu_encode(w2, cat(q), cat(k), cat(v))
+    cu2 = w2.cu_len
+    for j, r in enumerate(perm):
+        assert torch.equal(sl(out, r), out2[cu2[j]:cu2[j + 1]])
+        assert torch.equal(kc[:, cu[r]:cu[r + 1]], kc2[:, cu2[j]:cu2[j + 1]])
+        assert torch.equal(lse[:, cu[r]:cu[r + 1]], lse2[:, cu2[j]:cu2[j + 1]])
+    # new neighbour content
+    g = torch.Generator(device="cpu").manual_seed(99)
+    q3, k3, v3 = q.clone(), k.clone(), v.clone()
+    a, b = int(cu[1]), int(cu[2])
+    for t in (q3, k3, v3):
+        t[a:b] = torch.randn(t[a:b].shape, generator=g).to(t.dtype).to(DEV)
+    out3, kc3, _, _ = gpu_encode(w, q3, k3, v3)
+    for r in (0, 2, 3, 4):
+        assert torch.equal(sl(out, r), sl(out3, r))
+        assert torch.equal(kc[:, cu[r]:cu[r + 1]], kc3[:, cu[r]:cu[r + 1]])
+
+
+def test_encode_deterministic():
+    print_case("encode determinism")
+    w = config(2)["encode"]
+    q, k, v = w.tensors(DEV)
+    a = gpu_encode(w, q, k, v)
+    b = gpu_encode(w, q, k, v)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_config2_full_size_sampled_resources():
+    """Config 2 at full size (16 resources, 32/8 heads, d 128) in the
+    benchmark's launch configuration; the oracle recomputes whole resources
+    (shortest, longest and two more), each on its own, which the definition
+    allows: no attention crosses resources."""
+    print_case("config2 full")
+    w = config(2)["encode"]
+    q, k, v = w.tensors(DEV)
+    out, kc, vc, lse = gpu_encode(w, q, k, v)
+    cu = w.cu_len
+    picks = sorted({int(np.argmin(w.lengths)), int(np.argmax(w.lengths)), 3, 10})
+    for r in picks:
+        a, b = int(cu[r]), int(cu[r + 1])
+        ref = oracle.encode(q[a:b].cpu(), k[a:b].cpu(), v[a:b].cpu(), [0, b - a], w.rope_base)
+        check(out[a:b], ref["out"], "bf16", "out r%d" % r)
+        check(kc[:, a:b], ref["k_cache"], "bf16", "k_cache r%d" % r)
+        check(lse[:, a:b], ref["lse"], "bf16", "lse r%d" % r)
+        assert torch.equal(vc[:, a:b], v[a:b].permute(1, 0, 2))
+
+
+# ---------------------------------------------------------------- prune and routes
+
+@pytest.mark.parametrize("k", [4, 5])
+def test_routes_bitexact_full_size(k):
+    print_case("routes config", k)
+    a = config(k)["attend"]
+    rt = Routes(a)
+    torch.cuda.synchronize()
+    off, res, tok = oracle.routes(a.req_res_off, a.req_res, a.mask, a.cu_rows)
+    assert np.array_equal(rt.route_off.cpu().numpy(), off)
+    assert np.array_equal(rt.route_res.cpu().numpy()[: off[-1]], res)
+    assert np.array_equal(rt.route_tokens.cpu().numpy(), tok)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 128), ("f32", 64)])
+def test_prune_gather_bitexact(dtype, d):
+    print_case("prune", dtype, d)
+    a = config(4)["attend"]
+    T = int(a.cu_len[-1])
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    kc = normal((8, T, d), dt, 40, 1, DEV)
+    vc = normal((8, T, d), dt, 40, 2, DEV)
+    K = int(a.cu_kept[-1])
+    kk = torch.empty(8, K, d, dtype=dt, device=DEV)
+    vk = torch.empty_like(kk)
+    rc.prune_gather(kc, vc, i32(a.cu_len), i32(a.cu_kept), i32(a.kept_idx), kk, vk)
+    torch.cuda.synchronize()
+    rk, rv = oracle.prune(kc.cpu(), vc.cpu(), a.cu_len, a.cu_kept, a.kept_idx)
+    assert np.array_equal(oracle.host_view(kk.cpu()), rk)
+    assert np.array_equal(oracle.host_view(vk.cpu()), rv)
+
+
+def test_prune_extremes():
+    """Keep everything: identity.  Keep only the suffix token of each resource."""
+    print_case("prune extremes")
+    lengths = np.array([5, 1, 40, 7], np.int32)
+    cu = prefix(lengths)
+    kc = normal((2, int(cu[-1]), 128), torch.bfloat16, 41, 1, DEV)
+    vc = normal((2, int(cu[-1]), 128), torch.bfloat16, 41, 2, DEV)
+    full = np.concatenate([np.arange(n) for n in lengths]).astype(np.int32)
+    kk, vk = torch.empty_like(kc), torch.empty_like(vc)
+    rc.prune_gather(kc, vc, i32(cu), i32(cu), i32(full), kk, vk)
+    assert torch.equal(kk, kc) and torch.equal(vk, vc)
+    ks = torch.empty(2, 4, 128, dtype=torch.bfloat16, device=DEV)
+    vs = torch.empty_like(ks)
+    rc.prune_gather(kc, vc, i32(cu), i32(np.arange(5)), i32(lengths - 1), ks, vs)
+    assert torch.equal(ks, kc[:, torch.from_numpy(cu[1:] - 1).long().to(DEV)])
+
+
+# ---------------------------------------------------------------- attend (prefill and decode)
+
+def small_attend(seed, n_req, pool, Hq, Hkv, d, dtype, q_lens, ctx_lens, L=3, prune=True,
+                 mask_p=0.5, max_len=300):
+    rng = np.random.default_rng(seed)
+    lengths = draw_lengths(rng, pool, 1, max_len)
+    reqs = [rng.permutation(pool)[: rng.integers(0, pool + 1)] for _ in range(n_req)]
+    req_res_off = prefix([len(r) for r in reqs])
+    req_res = np.concatenate(reqs).astype(np.int32) if req_res_off[-1] else np.zeros(0, np.int32)
+    mask = (rng.random((pool, L, Hkv)) < mask_p).astype(np.uint8)
+    cu_kept = kept_idx = None
+    if prune:
+        cu_kept, kept_idx = draw_kept(rng, lengths, 0.3)
+    return AttendWorkload(seed=seed, n_layers=L, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d,
+                          dtype=dtype, lengths=lengths, req_res_off=req_res_off, req_res=req_res,
+                          q_lens=np.asarray(q_lens, np.int32), ctx_lens=np.asarray(ctx_lens, np.int32),
+                          mask=mask, cu_kept=cu_kept, kept_idx=kept_idx)
+
+
+def run_attend_case(w, layer, chain=False):
+    """GPU attend (optionally behind a GPU prune of unpruned caches) vs oracle."""
+    rt = Routes(w)
+    q, ck, cv, rk, rv = w.layer_tensors(layer, DEV, compacted=not chain)
+    if chain:
+        K = int(w.cu_kept[-1])
+        kk = torch.empty(w.n_kv_heads, K, w.head_dim, dtype=rk.dtype, device=DEV)
+        vk = torch.empty_like(kk)
+        rc.prune_gather(rk, rv, i32(w.cu_len), i32(w.cu_kept), i32(w.kept_idx), kk, vk)
+        grk, grv = kk, vk
+    else:
+        grk, grv = rk, rv
+    max_kv = rt.max_kv(layer)
+    ws = rt.workspace(max_kv)
+    out, lse = rt.attend(q, ck, cv, grk, grv, layer, workspace=ws, max_kv=max_kv)
+    torch.cuda.synchronize()
+    if chain:
+        rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, rk.cpu(), rv.cpu(),
+                                   w.cu_len, w.req_res_off, w.req_res, w.mask, layer,
+                                   cu_kept=w.cu_kept, kept_idx=w.kept_idx)
+    else:
+        rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, rk.cpu(), rv.cpu(),
+                                   w.cu_rows, w.req_res_off, w.req_res, w.mask, layer)
+    check(out, rout, w.dtype, "attend out")
+    check(lse, rlse.T, w.dtype, "attend lse")
+    return out
+
+
+PREFILL_CASES = [
+    # seed, n_req, pool, Hq, Hkv, d, q_lens, ctx_lens
+    (21, 3, 6, 32, 8, 128, [100, 1, 64], [130, 1, 200]),
+    (22, 2, 5, 8, 2, 64, [33, 97], [33, 150]),
+    (23, 4, 8, 16, 8, 128, [65, 2, 31, 128], [65, 40, 31, 300]),
+    (24, 2, 4, 64, 8, 128, [40, 90], [41, 90]),
+    (25, 2, 4, 8, 8, 128, [129, 5], [129, 300]),
+]
+
+
+@pytest.mark.parametrize("case", PREFILL_CASES)
+def test_attend_prefill_bf16(case):
+    seed, n_req, pool, Hq, Hkv, d, ql, cl = case
+    print_case("prefill", case)
+    w = small_attend(seed, n_req, pool, Hq, Hkv, d, "bf16", ql, cl)
+    for layer in range(w.n_layers):
+        run_attend_case(w, layer)
+
+
+def test_attend_prefill_chain_with_prune():
+    print_case("prefill chain")
+    w = small_attend(31, 3, 6, 32, 8, 128, "bf16", [50, 70, 3], [80, 70, 10])
+    run_attend_case(w, 1, chain=True)
+
+
+@pytest.mark.parametrize("mask_p", [-1.0, 2.0])
+def test_attend_all_zero_and_all_one_masks(mask_p):
+    """Omega = empty (context only) and Omega = everything."""
+    print_case("mask extremes", mask_p)
+    w = small_attend(32, 3, 5, 32, 8, 128, "bf16", [40, 64, 1], [100, 64, 9], mask_p=mask_p)
+    run_attend_case(w, 0)
+
+
+DECODE_CASES = [
+    (41, 5, 8, 32, 8, 128, [1, 1, 1, 1, 1], [1, 17, 300, 1200, 64]),
+    (42, 3, 6, 8, 2, 64, [1, 1, 1], [5, 700, 33]),
+    (43, 4, 10, 64, 8, 128, [1] * 4, [100, 2000, 1, 513]),
+    (44, 2, 4, 8, 8, 128, [1, 1], [250, 7]),
+    (45, 3, 30, 16, 8, 128, [1] * 3, [3000, 5, 800]),
+]
+
+
+@pytest.mark.parametrize("case", DECODE_CASES)
+def test_attend_decode_bf16(case):
+    seed, n_req, pool, Hq, Hkv, d, ql, cl = case
+    print_case("decode", case)
+    w = small_attend(seed, n_req, pool, Hq, Hkv, d, "bf16", ql, cl, max_len=900)
+    for layer in range(w.n_layers):
+        run_attend_case(w, layer)
+
+
+def test_attend_fp32_prefill_and_decode():
+    print_case("attend fp32")
+    w = small_attend(51, 3, 5, 8, 2, 128, "f32", [20, 1, 7], [20, 30, 40])
+    run_attend_case(w, 2)
+    w = small_attend(52, 2, 5, 8, 2, 64, "f32", [1, 1], [1, 90])
+    run_attend_case(w, 0, chain=True)
+
+
+def test_decode_deterministic():
+    print_case("decode determinism")
+    w = small_attend(46, 4, 8, 32, 8, 128, "bf16", [1] * 4, [900, 20, 3000, 64], max_len=900)
+    a = run_attend_case(w, 0)
+    b = run_attend_case(w, 0)
+    assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- full-size attend configs
+
+def sample_rows(w, per_req, seed):
+    rng = np.random.default_rng(seed)
+    rb, ri = [], []
+    for b in range(w.n_req):
+        Tq = int(w.q_lens[b])
+        pick = {0, Tq - 1} | set(rng.choice(Tq, size=min(per_req, Tq), replace=False).tolist())
+        for i in sorted(pick):
+            rb.append(b)
+            ri.append(i)
+    return np.array(rb, np.int32), np.array(ri, np.int32)
+
+
+@pytest.mark.parametrize("k,layers", [(3, [0, 35]), (4, [0, 17])])
+def test_prefill_full_size_sampled_rows(k, layers):
+    """Configs 3 / 4 at full size (8 requests x 2048 queries, 36-layer route
+    CSR, compacted KV for config 4), sampled query rows per request."""
+    w = config(k)["attend"]
+    rt = Routes(w)
+    for layer in layers:
+        print_case("prefill full", k, layer)
+        q, ck, cv, rk, rv = w.layer_tensors(layer, DEV)
+        out, lse = rt.attend(q, ck, cv, rk, rv, layer)
+        torch.cuda.synchronize()
+        rb, ri = sample_rows(w, 14, 100 + layer)
+        rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, rk.cpu(),
+                                   rv.cpu(), w.cu_rows, w.req_res_off, w.req_res, w.mask, layer,
+                                   rows=(rb, ri))
+        rows = torch.from_numpy(w.cu_q[rb] + ri).long().to(DEV)
+        check(out[rows], rout, "bf16", "out")
+        check(lse[:, rows], rlse.T, "bf16", "lse")
+
+
+def test_decode_full_size_layers():
+    """Config 5 at full size (64 requests over 32 resources each, 4096
+    context rows) for two layers, every output."""
+    w = config(5)["attend"]
+    rt = Routes(w)
+    for layer in (0, 23):
+        print_case("decode full", layer)
+        q, ck, cv, rk, rv = w.layer_tensors(layer, DEV)
+        mk = rt.max_kv(layer)
+        ws = rt.workspace(mk)
+        out, lse = rt.attend(q, ck, cv, rk, rv, layer, workspace=ws, max_kv=mk)
+        torch.cuda.synchronize()
+        rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, rk.cpu(),
+                                   rv.cpu(), w.cu_rows, w.req_res_off, w.req_res, w.mask, layer)
+        check(out, rout, "bf16", "out")
+        check(lse, rlse.T, "bf16", "lse")
+        del q, ck, cv, rk, rv
+        torch.cuda.empty_cache()
