@@ -93,8 +93,22 @@ def _check(rc, what):
         raise ValueError("oracle_%s rejected its arguments" % what)
 
 
-def rope(x, pos, base: float) -> np.ndarray:
-    """RoPE of x[T][H][d] at positions pos[T]; returns float64 [T][H][d]."""
+def _rot(x, rot_dtype):
+    return _dtype_code(x) if rot_dtype is None else int(rot_dtype)
+
+
+def round_to(x, dtype: int) -> np.ndarray:
+    """Round float64 values to nearest-even at the precision of dtype (F32/BF16/F64)."""
+    x = np.ascontiguousarray(np.asarray(x, np.float64))
+    f = _load().oracle_round
+    f.restype = ctypes.c_double
+    f.argtypes = [ctypes.c_double, ctypes.c_int]
+    return np.array([f(float(v), int(dtype)) for v in x.ravel()]).reshape(x.shape)
+
+
+def rope(x, pos, base: float, rot_dtype=None) -> np.ndarray:
+    """RoPE of x[T][H][d] at positions pos[T]; returns float64 [T][H][d] whose
+    values are rounded to the precision of rot_dtype (default: x's dtype)."""
     x = host_view(x)
     pos = _i32(pos)
     T, H, d = x.shape
@@ -102,16 +116,20 @@ def rope(x, pos, base: float) -> np.ndarray:
     lib = _load()
     lib.oracle_rope.restype = ctypes.c_int
     rc = lib.oracle_rope(ctypes.c_int(_dtype_code(x)), ctypes.c_int(T), ctypes.c_int(H),
-                         ctypes.c_int(d), ctypes.c_double(base), _p(pos), _p(x), _p(y))
+                         ctypes.c_int(d), ctypes.c_double(base), _p(pos), _p(x), _p(y),
+                         ctypes.c_int(_rot(x, rot_dtype)))
     _check(rc, "rope")
     return y
 
 
-def encode(q, k, v, cu_len, base: float, scale: float | None = None, pos_base=None):
+def encode(q, k, v, cu_len, base: float, scale: float | None = None, pos_base=None,
+           rot_dtype=None):
     """Block-diagonal causal encode of packed resources (one layer).
 
-    q[T][Hq][d], k/v[T][Hkv][d] in stored precision.  Returns a dict of
-    float64 arrays: out[T][Hq][d], k_cache/v_cache[Hkv][T][d], lse[Hq][T].
+    q[T][Hq][d], k/v[T][Hkv][d] in stored precision.  Rotated queries and keys
+    are rounded to the precision of rot_dtype (default: the inputs' dtype).
+    Returns a dict of float64 arrays: out[T][Hq][d], k_cache/v_cache[Hkv][T][d],
+    lse[Hq][T].
     """
     q, k, v = host_view(q), host_view(k), host_view(v)
     cu_len = _i32(cu_len)
@@ -129,7 +147,7 @@ def encode(q, k, v, cu_len, base: float, scale: float | None = None, pos_base=No
         ctypes.c_int(_dtype_code(q)), ctypes.c_int(len(cu_len) - 1), _p(cu_len),
         ctypes.c_int(Hq), ctypes.c_int(Hkv), ctypes.c_int(d), ctypes.c_double(base),
         _p(pos_base), ctypes.c_double(scale), _p(q), _p(k), _p(v),
-        _p(out), _p(kc), _p(vc), _p(lse))
+        _p(out), _p(kc), _p(vc), _p(lse), ctypes.c_int(_rot(q, rot_dtype)))
     _check(rc, "encode")
     return {"out": out, "k_cache": kc, "v_cache": vc, "lse": lse}
 

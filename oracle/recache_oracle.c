@@ -70,6 +70,21 @@ static size_t elem_size(int dtype) {
     return dtype == ORACLE_F64 ? 8 : dtype == ORACLE_F32 ? 4 : 2;
 }
 
+/* Round to nearest, ties to even, to the precision of a storage dtype: fp64
+ * unchanged, fp32 via the C conversion (round-to-nearest-even), bf16 to 8
+ * significant bits.  Rotated queries and keys are held at the workload's
+ * storage precision, as a backbone running in that precision holds them (the
+ * key cache is stored in it); everything after that is fp64. */
+static double round_to(double x, int dtype) {
+    if (dtype == ORACLE_F64 || x == 0.0 || !isfinite(x)) return x;
+    if (dtype == ORACLE_F32) return (double)(float)x;
+    int e;
+    double m = frexp(x, &e);          /* x = m 2^e, 0.5 <= |m| < 1 */
+    return ldexp(rint(ldexp(m, 8)), e - 8);  /* 8 significant bits, ties to even */
+}
+
+double oracle_round(double x, int dtype) { return round_to(x, dtype); }
+
 /* ------------------------------------------------------------------------ */
 /* RoPE (half-split).  For i in [0, d/2): theta_i = base^(-2i/d),
  * y_i       = x_i cos(p theta_i) - x_{i+d/2} sin(p theta_i)
@@ -85,16 +100,19 @@ void oracle_rope_vec(const double* x, double* y, int d, double base, double pos)
     }
 }
 
-/* Rotate x[T][H][d] (stored dtype) at positions pos[T]; y[T][H][d] double. */
+/* Rotate x[T][H][d] (stored dtype) at positions pos[T]; y[T][H][d] double,
+ * each value rounded to the precision of rot_dtype. */
 int oracle_rope(int dtype, int T, int H, int d, double base, const int32_t* pos,
-                const void* x, double* y) {
-    if (T < 0 || H <= 0 || d <= 0 || (d % 2) || !pos || (T && (!x || !y))) return -1;
+                const void* x, double* y, int rot_dtype) {
+    if (T < 0 || H <= 0 || d <= 0 || d > 512 || (d % 2) || !pos || (T && (!x || !y))) return -1;
 #pragma omp parallel for schedule(static)
     for (long th = 0; th < (long)T * H; ++th) {
         long t = th / H;
         double xv[512];
         for (int e = 0; e < d; ++e) xv[e] = widen(x, dtype, (size_t)th * d + e);
-        oracle_rope_vec(xv, y + (size_t)th * d, d, base, (double)pos[t]);
+        double* yr = y + (size_t)th * d;
+        oracle_rope_vec(xv, yr, d, base, (double)pos[t]);
+        for (int e = 0; e < d; ++e) yr[e] = round_to(yr[e], rot_dtype);
     }
     return 0;
 }
@@ -129,6 +147,9 @@ static double softmax_average(const double* z, int n, int d, vrow_fn vrow, void*
  * Query row t of resource r, head h, attends keys u in [cu_len[r], t] of KV
  * head h / (Hq / Hkv), with logits scale * <RoPE(q_t), RoPE(k_u)>.
  *
+ * Rotated queries and keys are rounded to the precision of rot_dtype (the
+ * workload's storage dtype; fp64 keeps them exact).
+ *
  * Outputs (double): out[T][Hq][d]; k_cache[Hkv][T][d] holds the rotated keys
  * and v_cache[Hkv][T][d] the values (head-major); lse[Hq][T] (optional)
  * holds the natural-log sum-exp of the scaled logits.                      */
@@ -142,7 +163,7 @@ static const double* enc_vrow(void* c, int u, double* scratch) {
 int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, int d,
                   double base, const int32_t* pos_base, double scale,
                   const void* q, const void* k, const void* v,
-                  double* out, double* k_cache, double* v_cache, double* lse) {
+                  double* out, double* k_cache, double* v_cache, double* lse, int rot_dtype) {
     if (n_res <= 0 || !cu_len || Hq <= 0 || Hkv <= 0 || Hq % Hkv || d <= 0 || d > 512 ||
         (d % 2) || !q || !k || !v || !out || !k_cache || !v_cache)
         return -1;
@@ -165,7 +186,9 @@ int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, 
         double p = (double)((pos_base ? pos_base[r] : 0) + (t - cu_len[r]));
         double xv[512];
         for (int e = 0; e < d; ++e) xv[e] = widen(k, dtype, ((size_t)t * Hkv + g) * d + e);
-        oracle_rope_vec(xv, k_cache + ((size_t)g * T + t) * d, d, base, p);
+        double* kr = k_cache + ((size_t)g * T + t) * d;
+        oracle_rope_vec(xv, kr, d, base, p);
+        for (int e = 0; e < d; ++e) kr[e] = round_to(kr[e], rot_dtype);
         for (int e = 0; e < d; ++e)
             v_cache[((size_t)g * T + t) * d + e] = widen(v, dtype, ((size_t)t * Hkv + g) * d + e);
     }
@@ -183,6 +206,7 @@ int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, 
             double p = (double)((pos_base ? pos_base[r] : 0) + j);
             for (int e = 0; e < d; ++e) qv[e] = widen(q, dtype, ((size_t)t * Hq + h) * d + e);
             oracle_rope_vec(qv, qr, d, base, p);
+            for (int e = 0; e < d; ++e) qr[e] = round_to(qr[e], rot_dtype);
             for (int u = 0; u <= j; ++u) {
                 const double* kr = k_cache + ((size_t)g * T + o + u) * d;
                 double dot = 0.0;

@@ -325,12 +325,14 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         for (int s = 0; s < 4; ++s) {
             float p[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                p[e] = exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
-                lsum += p[e];
-            }
+            for (int e = 0; e < 8; ++e) p[e] = exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
             u32x4 w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                        pack_bf16x2(p[6], p[7])};
+            // normalise by the weights as rounded for the P V product, so that
+            // the output is an exact weighted mean of the V rows it used
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                lsum += __uint_as_float(w[i] << 16) + __uint_as_float(w[i] & 0xffff0000u);
             pf[s] = __builtin_bit_cast(bf16x8, w);
         }
 #pragma unroll

@@ -39,12 +39,31 @@ __device__ __forceinline__ float row_sum(float x) {
     return x;
 }
 
+// acc + sum of the 8 products of two rows of 8 bf16 (fp32 accumulation).
+// The dwords are taken out of the 16-byte vectors first: handed the vector
+// elements directly, the compiler's dot2 lowering reads the first dword four
+// times.
 __device__ __forceinline__ float dot8_bf16(const u32x4& k, const u32x4& q, float acc) {
+    const uint32_t ks[4] = {k.x, k.y, k.z, k.w}, qs[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
     for (int w = 0; w < 4; ++w)
-        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, k[w]),
-                                              __builtin_bit_cast(bf16x2, q[w]), acc, false);
+        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, ks[w]),
+                                              __builtin_bit_cast(bf16x2, qs[w]), acc, false);
     return acc;
+}
+
+// One row's R logits into LDS with a single vector store.
+template <int R>
+__device__ __forceinline__ void store_row(float* dst, const float* v) {
+    if constexpr (R == 1) {
+        dst[0] = v[0];
+    } else if constexpr (R == 2) {
+        *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < R; j += 4)
+            *reinterpret_cast<float4*>(dst + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+    }
 }
 
 template <int HD, int R>
@@ -52,7 +71,7 @@ struct DecSmem {
     int seg_start[kMaxSeg + 1];
     int seg_row[kMaxSeg];
     int scan[kThreads];
-    float sc[kSub * R];        // logits, then weights, [row][head]
+    alignas(16) float sc[kSub * R];  // logits, then weights, [row][head]
     float red[4][R];           // per-wave maxima
     float bm[R];               // block running max (log2 units)
     float ored[4][R][HD];      // cross-wave O reduction
@@ -177,12 +196,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
             for (int u = 0; u < UNR; ++u) {
                 const int i = i0 + u * RPB;
                 if (i < n) {
+                    float sv[R];
 #pragma unroll
                     for (int h = 0; h < R; ++h) {
-                        const float s2 = row_sum<LPR>(dot8_bf16(kr[u], qv[h], 0.f)) * sl2;
-                        mloc[h] = fmaxf(mloc[h], s2);
-                        if (c == h) sm.sc[i * R + h] = s2;
+                        sv[h] = row_sum<LPR>(dot8_bf16(kr[u], qv[h], 0.f)) * sl2;
+                        mloc[h] = fmaxf(mloc[h], sv[h]);
                     }
+                    if (c == 0) store_row<R>(&sm.sc[i * R], sv);
                 }
             }
         }

@@ -63,8 +63,20 @@ def dense_masked_attention(q, k, v, M, scale):
     return (w @ v) / den, (m + np.log(den))[:, 0]
 
 
+def rne_bits(x: np.ndarray, mant_bits: int) -> np.ndarray:
+    """Round float64 values to nearest-even with mant_bits explicit mantissa
+    bits (7 for bf16, 23 for fp32), by integer arithmetic on the IEEE bits."""
+    x = np.ascontiguousarray(np.asarray(x, np.float64))
+    b = x.view(np.uint64).copy()
+    drop = np.uint64(52 - mant_bits)
+    lsb = (b >> drop) & np.uint64(1)
+    b = b + ((np.uint64(1) << (drop - np.uint64(1))) - np.uint64(1)) + lsb
+    b &= ~((np.uint64(1) << drop) - np.uint64(1))
+    return b.view(np.float64)
+
+
 def request(res_q, res_k, res_v, ctx_q, ctx_k, ctx_v, ctx_pos, kept, route_bits_lg, base,
-            scale, n_q):
+            scale, n_q, round_rot=None):
     """One request, one layer.
 
     res_q/res_k/res_v: lists (request order) of raw [D][Hq|Hkv][d] arrays;
@@ -73,7 +85,8 @@ def request(res_q, res_k, res_v, ctx_q, ctx_k, ctx_v, ctx_pos, kept, route_bits_
     in this layer; n_q: the last n_q context tokens are the queries.
 
     Returns (res_out[D_R][Hq][d], ctx_out[n_q][Hq][d], res_lse[D_R][Hq],
-    ctx_lse[n_q][Hq], mask_popcount_per_group[G]).
+    ctx_lse[n_q][Hq], mask_popcount_per_group[G]).  round_rot, if given, is
+    applied to the rotated queries and keys.
     """
     lengths = [a.shape[0] for a in res_q]
     Tc = ctx_q.shape[0]
@@ -85,6 +98,8 @@ def request(res_q, res_k, res_v, ctx_q, ctx_k, ctx_v, ctx_pos, kept, route_bits_
     K = np.concatenate(list(res_k) + [ctx_k], axis=0).astype(np.float64)
     V = np.concatenate(list(res_v) + [ctx_v], axis=0).astype(np.float64)
     Qr, Kr = rope_complex(Q, pos, base), rope_complex(K, pos, base)
+    if round_rot is not None:  # rotated Q / K held at a storage precision
+        Qr, Kr = round_rot(Qr), round_rot(Kr)
     N, DR = Q.shape[0], sum(lengths)
     out = np.zeros((N, Hq, d))
     lse = np.zeros((N, Hq))

@@ -3,10 +3,16 @@ the route build, and the tolerance rules.
 
 Tolerances (stated once, used by every GPU test):
   fp32 inputs:  |gpu - oracle| <= 1e-5 everywhere.
-  bf16 inputs:  |gpu - oracle| <= 1e-2 + 2^-9 |oracle| everywhere: the 1e-2
+  bf16 inputs:  |gpu - oracle| <= 1e-2 + 2^-8 |oracle| everywhere: the 1e-2
                 bound for fp32 accumulation over bf16 inputs, widened by the
-                half-ulp of rounding the output to bf16 (a correctly rounded
-                bf16 value of magnitude in [4, 8) can be 2^-6 away).
+                half-ulp of rounding the output to bf16 (at most 2^-8 of the
+                value: bf16 keeps 8 significant bits).  The oracle holds
+                rotated queries and keys at bf16, as the kernels and a bf16
+                backbone do; rotated values written in bf16 (the K cache,
+                rotated queries) must then match the oracle's to one bf16 ulp
+                plus the absolute error of the fp32 rotation before rounding:
+                <= 2^-7 |oracle| + 1e-5 (the absolute term matters where the
+                two products of a rotation cancel).
   index work:   bit-exact.
 """
 from __future__ import annotations
@@ -35,11 +41,18 @@ def check(gpu, ref, dtype: str, name: str):
     err = np.abs(g - ref)
     if dtype == "f32":
         bound = np.full_like(ref, 1e-5)
+    elif dtype == "bf16-ulp":
+        bound = 2.0 ** -7 * np.abs(ref) + 1e-5
     else:
-        bound = 1e-2 + 2.0 ** -9 * np.abs(ref)
+        bound = 1e-2 + 2.0 ** -8 * np.abs(ref)
     bad = ~(err <= bound)
-    assert not bad.any(), "%s: %d of %d out of tolerance, max abs err %.3g at %s" % (
-        name, int(bad.sum()), bad.size, float(np.nanmax(err)), np.argwhere(bad)[0].tolist())
+    if bad.any():
+        ratio = np.where(np.isnan(err), np.inf, err / bound)
+        worst = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
+        raise AssertionError("%s: %d of %d out of tolerance; worst at %s: gpu %r, oracle %r, bound %.3g"
+                             " (max abs err %.3g)" % (name, int(bad.sum()), bad.size, list(worst),
+                                                      g[worst], ref[worst], bound[worst],
+                                                      float(np.nanmax(err))))
     return float(err.max()) if err.size else 0.0
 
 

@@ -49,7 +49,7 @@ def test_config1_end_to_end(dtype):
     out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
     ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
     check(out, ref["out"], dtype, "encode out")
-    check(kc, ref["k_cache"], dtype, "k_cache")
+    check(kc, ref["k_cache"], "f32" if dtype == "f32" else "bf16-ulp", "k_cache")
     assert torch.equal(vc.cpu(), v.permute(1, 0, 2).contiguous())
     check(lse, ref["lse"], "f32" if dtype == "f32" else "bf16", "encode lse")
 
@@ -69,10 +69,10 @@ def test_config1_end_to_end(dtype):
     torch.cuda.synchronize()
     rq = oracle.rope(cq, pos, 1e4)
     rk = oracle.rope(ckr, pos, 1e4)
-    check(gq, rq, dtype, "rope_q")
-    check(gck, rk.transpose(1, 0, 2), dtype, "rope_kv")
+    check(gq, rq, "f32" if dtype == "f32" else "bf16-ulp", "rope_q")
+    check(gck, rk.transpose(1, 0, 2), "f32" if dtype == "f32" else "bf16-ulp", "rope_kv")
     rout, rlse = oracle.attend(rq, np.ascontiguousarray(rk.transpose(1, 0, 2)),
-                               oracle.host_view(cvr).transpose(1, 0, 2).astype(np.float64).copy(),
+                               cvr.permute(1, 0, 2).contiguous().double().numpy(),
                                a.cu_q, a.cu_ctx, ref["k_cache"], ref["v_cache"], a.cu_len,
                                a.req_res_off, a.req_res, a.mask, 0)
     check(gout, rout, dtype, "attend out")
@@ -94,7 +94,7 @@ def test_encode_bf16_ragged(Hq, Hkv, d):
     out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
     ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
     check(out, ref["out"], "bf16", "out")
-    check(kc, ref["k_cache"], "bf16", "k_cache")
+    check(kc, ref["k_cache"], "bf16-ulp", "k_cache")
     check(lse, ref["lse"], "bf16", "lse")
     # first token of every resource sees only itself: its output is its V row exactly
     vv = v.to(DEV)
@@ -115,7 +115,7 @@ def test_encode_pos_base_shift():
     out, kc, _, _ = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV), pos_base=pb)
     ref = oracle.encode(q, k, v, w.cu_len, w.rope_base, pos_base=pb)
     check(out, ref["out"], "bf16", "out")
-    check(kc, ref["k_cache"], "bf16", "k_cache")
+    check(kc, ref["k_cache"], "bf16-ulp", "k_cache")
 
 
 def test_encode_composition_invariance_bitexact():
@@ -176,7 +176,7 @@ def test_config2_full_size_sampled_resources():
         a, b = int(cu[r]), int(cu[r + 1])
         ref = oracle.encode(q[a:b].cpu(), k[a:b].cpu(), v[a:b].cpu(), [0, b - a], w.rope_base)
         check(out[a:b], ref["out"], "bf16", "out r%d" % r)
-        check(kc[:, a:b], ref["k_cache"], "bf16", "k_cache r%d" % r)
+        check(kc[:, a:b], ref["k_cache"], "bf16-ulp", "k_cache r%d" % r)
         check(lse[:, a:b], ref["lse"], "bf16", "lse r%d" % r)
         assert torch.equal(vc[:, a:b], v[a:b].permute(1, 0, 2))
 

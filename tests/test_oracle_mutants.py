@@ -47,9 +47,19 @@ MUTANTS = {
     "vcache_from_k": ("v_cache[((size_t)g * T + t) * d + e] = widen(v, dtype,",
                       "v_cache[((size_t)g * T + t) * d + e] = widen(k, dtype,"),
     "softmax_no_normalise": ("for (int e = 0; e < d; ++e) out[e] /= denom;", ""),
+    "round_truncates": ("return ldexp(rint(ldexp(m, 8)), e - 8);",
+                        "return ldexp(trunc(ldexp(m, 8)), e - 8);"),
+    "round_keeps_9_bits": ("return ldexp(rint(ldexp(m, 8)), e - 8);",
+                           "return ldexp(rint(ldexp(m, 9)), e - 9);"),
+    "encode_query_not_rounded": ("for (int e = 0; e < d; ++e) qr[e] = round_to(qr[e], rot_dtype);",
+                                 ""),
+    "rope_not_rounded": ("for (int e = 0; e < d; ++e) yr[e] = round_to(yr[e], rot_dtype);", ""),
 }
 
 PINS = [
+    pins.test_round_to_bf16_tie_cases_and_bit_level_rne,
+    pins.test_rope_rounds_to_storage_precision,
+    pins.test_encode_bf16_storage_precision_matches_bruteforce,
     pins.test_rope_d2_closed_form,
     pins.test_rope_matches_complex_form_and_identities,
     pins.test_encode_single_resource_is_textbook_causal_attention,

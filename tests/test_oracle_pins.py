@@ -82,6 +82,31 @@ def test_widening_is_exact():
     assert np.array_equal(oracle.rope(t32, np.zeros(4, np.int32), 1e4), t32.double().numpy())
 
 
+def test_round_to_bf16_tie_cases_and_bit_level_rne():
+    """Storage-precision rounding: hand-worked ties, then an independent
+    bit-level round-to-nearest-even on random and tie-heavy values."""
+    x = np.array([1 + 2.0**-8, 1 + 3 * 2.0**-8, 1 + 2.0**-8 + 2.0**-20, -1.5, 255.5, 0.0,
+                  -(1 + 2.0**-8)])
+    want = np.array([1.0, 1 + 2.0**-6, 1 + 2.0**-7, -1.5, 256.0, 0.0, -1.0])
+    assert np.array_equal(oracle.round_to(x, oracle.BF16), want)
+    rng = np.random.default_rng(3)
+    r = rng.standard_normal(4000) * 10.0 ** rng.integers(-3, 4, 4000)
+    ties = (rng.integers(1, 255, 2000) * 2 + 1) * 2.0 ** -9 + rng.integers(1, 4, 2000)
+    for v in (r, ties, -ties):
+        assert np.array_equal(oracle.round_to(v, oracle.BF16), bf.rne_bits(v, 7))
+        assert np.array_equal(oracle.round_to(v, oracle.F32), bf.rne_bits(v, 23))
+        assert np.array_equal(oracle.round_to(v, oracle.F64), v)
+
+
+def test_rope_rounds_to_storage_precision():
+    t = torch.randn(30, 2, 64).to(torch.bfloat16)
+    pos = np.arange(30, dtype=np.int32) * 37 + 5
+    y = oracle.rope(t, pos, 1e4)
+    exact = bf.rope_complex(t.double().numpy(), pos, 1e4)
+    assert np.array_equal(y, bf.rne_bits(exact, 7))
+    assert np.max(np.abs(oracle.rope(t, pos, 1e4, rot_dtype=oracle.F64) - exact)) < 1e-12
+
+
 # ------------------------------------------------------------------ encode
 
 def sdpa_causal(qr, kr, v, scale, ratio):
@@ -118,6 +143,26 @@ def test_encode_blockdiag_matches_bruteforce_and_lse():
         [None] * len(res), [[1, 1]] * len(res), t.base, 1 / 4.0, 1)
     assert np.max(np.abs(enc["out"] - bro)) < 1e-12
     assert np.max(np.abs(enc["lse"].T - brl)) < 1e-12
+
+
+def test_encode_bf16_storage_precision_matches_bruteforce():
+    """bf16 inputs: rotated Q / K are held at bf16 (nearest even), the rest is
+    exact; the brute force applies the same rounding by bit arithmetic."""
+    t = make_tiny(7, n_res=4, Hq=4, Hkv=2, d=16, max_len=12)
+    qb, kb, vb = (torch.from_numpy(a).to(torch.bfloat16) for a in (t.q, t.k, t.v))
+    enc = oracle.encode(qb, kb, vb, t.cu_len, t.base)
+    res = np.arange(len(t.lengths))
+    cu = t.cu_len
+    d64 = lambda x: x.double().numpy()
+    bro, _, _, _, _ = bf.request(
+        [d64(qb)[cu[r]:cu[r + 1]] for r in res], [d64(kb)[cu[r]:cu[r + 1]] for r in res],
+        [d64(vb)[cu[r]:cu[r + 1]] for r in res], t.ctx_q[0], t.ctx_k[0], t.ctx_v[0],
+        t.ctx_pos[0], [None] * len(res), [[1, 1]] * len(res), t.base, 0.25, 1,
+        round_rot=lambda a: bf.rne_bits(a, 7))
+    assert np.max(np.abs(enc["out"] - bro)) < 1e-12
+    kr = bf.rne_bits(bf.rope_complex(d64(kb), np.concatenate([np.arange(n) for n in t.lengths]),
+                                     t.base), 7)
+    assert np.array_equal(enc["k_cache"], head_major(kr))
 
 
 def test_encode_first_token_is_its_value_row():
