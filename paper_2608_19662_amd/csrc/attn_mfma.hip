@@ -20,10 +20,10 @@
 // so every lane owns exactly one query row in both accumulators: row max and
 // row sum need one cross-lane step (lanes l and l^32), and the rescale of O is
 // lane-local.  K / V tiles of 64 keys are staged through LDS, double buffered
-// (global loads of tile t+1 are in flight while tile t is computed).  K is
-// stored row-major with an XOR swizzle of its 16-byte chunks; V is stored
-// transposed, with keys permuted inside each 16-key group so that the P^T
-// operand can be taken from the accumulator registers as they are.
+// (global loads of tile t+1 are in flight while tile t is computed).  Both
+// tiles are stored row-major with an XOR swizzle of their 16-byte chunks; the
+// V^T operand is read with gfx950's LDS transpose reads, in the key order in
+// which the S^T accumulator hands P^T to the second product.
 //
 // Tiles never cross a resource boundary in encode, and the reduction order
 // depends only on local indices, so a resource's outputs are bit-identical
@@ -35,15 +35,8 @@ namespace rc {
 
 namespace {
 
-constexpr int kBK = 64;        // keys per tile
-constexpr int kVTS = kBK + 8;  // V^T row stride in bf16 (144 B: conflict-free 16 B reads)
+constexpr int kBK = 64;  // keys per tile
 constexpr int kThreads = 256;
-
-// Position of key k (0..63) inside the V^T row: bits 2 and 3 swapped, which is
-// the order in which the S^T accumulator hands keys to the P^T operand.
-__device__ __forceinline__ int vt_slot(int k) {
-    return (k & ~15) | (((k >> 2) & 1) << 3) | (((k >> 3) & 1) << 2) | (k & 3);
-}
 
 template <int HD>
 struct Tile {
@@ -51,12 +44,15 @@ struct Tile {
     static constexpr int KPT = kBK * CPR / kThreads;  // keys per thread per tile (4 or 2)
     static constexpr int NT = HD / 16;              // MFMA k-steps over head_dim
     static constexpr int NDB = HD / 32;             // 32-wide blocks of head_dim
-    static constexpr int K_ELEMS = kBK * HD;
-    static constexpr int V_ELEMS = HD * kVTS;
-    static constexpr int STAGE = K_ELEMS + V_ELEMS;  // bf16 elements per stage
+    static constexpr int STAGE = 2 * kBK * HD;      // bf16 elements per stage (K + V)
 };
 
 constexpr int kMaxSeg = 1024;
+
+template <int C>
+struct StageTag {
+    static constexpr int value = C;
+};
 
 template <int HD, bool ENCODE>
 struct Smem {
@@ -202,11 +198,45 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         for (int t = 0; t < TL::NT; ++t) qf[t] = __builtin_bit_cast(bf16x8, raw[t]);
     }
 
-    // ---- K/V tile staging.  Thread owns keys kq*KPT + [0, KPT), chunk c.
+    // ---- K / V tiles in LDS, both row-major [64 keys][HD] with the 16-byte
+    // chunks of each row XOR-swizzled by the key's low bits, double buffered.
+    constexpr int ROWB = HD * 2;
+    constexpr int TILEB = kBK * ROWB;
+    constexpr int STAGEB = 2 * TILEB;  // K tile, then V tile
+    char* lds = reinterpret_cast<char*>(sm.kv);
+    auto swz = [](int row, int chunk) -> uint32_t {
+        return (uint32_t)(row * ROWB + ((chunk ^ (row % TL::CPR)) << 4));
+    };
+
+    // Staging: thread owns keys kq*KPT + [0, KPT) at chunk c (coalesced rows).
     const int c = tid % TL::CPR;
     const int kq = tid / TL::CPR;
-    u32x4 kreg[TL::KPT], vreg[TL::KPT];
+    uint32_t st_off[TL::KPT];
+#pragma unroll
+    for (int j = 0; j < TL::KPT; ++j) st_off[j] = swz(kq * TL::KPT + j, c);
+    // S^T operand A = K rows: key l32 (+32 for the second block), chunk 2t + half.
+    uint32_t k_rd[TL::NT];
+#pragma unroll
+    for (int t = 0; t < TL::NT; ++t) k_rd[t] = swz(l32, 2 * t + half);
+    // O^T operand A = V^T via transpose reads.  In a 16-lane group G, lane i
+    // receives element i % 4 of the 8-byte pieces addressed by lanes 4k + i / 4
+    // (k = 0..3); pointing lane 4k + q at row r0 + k, column c0 + 4q hands lane
+    // i the column c0 + i of four consecutive rows.  Rows s*16 + w*8 + half*4
+    // + [0, 4) are the keys that the P^T operand holds in slots w*4 + [0, 4).
+    uint32_t v_rd[TL::NDB][2];
+    {
+        const int G = lane >> 4, i = lane & 15;
+#pragma unroll
+        for (int db = 0; db < TL::NDB; ++db)
+#pragma unroll
+            for (int w = 0; w < 2; ++w) {
+                const int row = w * 8 + (G >> 1) * 4 + (i >> 2);
+                const int col = db * 32 + (G & 1) * 16 + (i & 3) * 4;
+                v_rd[db][w] = TILEB + swz(row, col >> 3) + (col & 7) * 2;
+            }
+    }
 
+    u32x4 kreg[TL::KPT], vreg[TL::KPT];
     auto row_ptr_off = [&](int p, const uint16_t*& kp, const uint16_t*& vp) {
         p = min(p, stream - 1);
         if constexpr (ENCODE) {
@@ -242,46 +272,29 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             vreg[j] = *reinterpret_cast<const u32x4*>(vp + c * 8);
         }
     };
-    auto store_tile = [&](int buf) {
-        uint16_t* ks = sm.kv + buf * TL::STAGE;
-        uint16_t* vt = ks + TL::K_ELEMS;
+    auto store_tile = [&](char* stage) {
 #pragma unroll
         for (int j = 0; j < TL::KPT; ++j) {
-            const int key = kq * TL::KPT + j;
-            *reinterpret_cast<u32x4*>(ks + key * HD + ((c ^ (key % TL::CPR)) * 8)) = kreg[j];
-        }
-        const int slot = vt_slot(kq * TL::KPT);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int d = c * 8 + i;
-            const int sh = 16 * (i & 1);
-            if constexpr (TL::KPT == 4) {
-                const uint32_t w0 = ((vreg[0][i >> 1] >> sh) & 0xffffu) | (((vreg[1][i >> 1] >> sh) & 0xffffu) << 16);
-                const uint32_t w1 = ((vreg[2][i >> 1] >> sh) & 0xffffu) | (((vreg[3][i >> 1] >> sh) & 0xffffu) << 16);
-                *reinterpret_cast<uint2*>(vt + d * kVTS + slot) = make_uint2(w0, w1);
-            } else {
-                const uint32_t w0 = ((vreg[0][i >> 1] >> sh) & 0xffffu) | (((vreg[1][i >> 1] >> sh) & 0xffffu) << 16);
-                *reinterpret_cast<uint32_t*>(vt + d * kVTS + slot) = w0;
-            }
+            *reinterpret_cast<u32x4*>(stage + st_off[j]) = kreg[j];
+            *reinterpret_cast<u32x4*>(stage + TILEB + st_off[j]) = vreg[j];
         }
     };
 
     load_tile(0);
-    store_tile(0);
+    store_tile(lds);
     __syncthreads();
 
     const float sl2 = a.scale_log2;
     float m = -INFINITY;  // running max of raw logits for this lane's row
-    float lsum = 0.f;     // this lane's partial sum of exp2 weights
+    float lsum = 0.f;     // this lane's partial sum of the (bf16-rounded) weights
     f32x16 oacc[TL::NDB];
 #pragma unroll
     for (int db = 0; db < TL::NDB; ++db) oacc[db] = f32x16{};
-
     const int lim = off + my_q;  // keys p <= lim are visible to this lane's row
-    for (int kt = 0; kt < n_tiles; ++kt) {
-        const int cur = kt & 1;
-        const uint16_t* ks = sm.kv + cur * TL::STAGE;
-        const uint16_t* vt = ks + TL::K_ELEMS;
+
+    auto tile = [&](auto stage_tag, int kt) {
+        constexpr int cur = decltype(stage_tag)::value;
+        const char* st = lds + cur * STAGEB;
         if (kt + 1 < n_tiles) load_tile(kt + 1);
 
         f32x16 sacc[2] = {f32x16{}, f32x16{}};
@@ -289,9 +302,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         for (int t = 0; t < TL::NT; ++t) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
-                const int key = kb * 32 + l32;
-                const int chunk = (t * 2 + half) ^ (key % TL::CPR);
-                const bf16x8 av = *reinterpret_cast<const bf16x8*>(ks + key * HD + chunk * 8);
+                const bf16x8 av = *reinterpret_cast<const bf16x8*>(st + k_rd[t] + kb * 32 * ROWB);
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[t], sacc[kb], 0, 0, 0);
             }
         }
@@ -313,7 +324,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         mt = pair_max(mt);
         const float m_new = fmaxf(m, mt);
         if (__builtin_amdgcn_ballot_w64(m_new > m)) {
-            const float alpha = exp2f((m - m_new) * sl2);  // 0 when m == -inf
+            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
             lsum *= alpha;
 #pragma unroll
             for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
@@ -325,7 +336,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         for (int s = 0; s < 4; ++s) {
             float p[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) p[e] = exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
+            for (int e = 0; e < 8; ++e)
+                p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
             u32x4 w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
                        pack_bf16x2(p[6], p[7])};
             // normalise by the weights as rounded for the P V product, so that
@@ -339,12 +351,22 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         for (int db = 0; db < TL::NDB; ++db) {
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
-                const bf16x8 av = *reinterpret_cast<const bf16x8*>(vt + (db * 32 + l32) * kVTS + s * 16 + half * 8);
+                typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4*)(st + v_rd[db][0] + s * 16 * ROWB));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_s16x4*)(st + v_rd[db][1] + s * 16 * ROWB));
+                const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+                const bf16x8 av = __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
                 oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pf[s], oacc[db], 0, 0, 0);
             }
         }
-        if (kt + 1 < n_tiles) store_tile(cur ^ 1);
+        if (kt + 1 < n_tiles) store_tile(lds + (cur ^ 1) * STAGEB);
         __syncthreads();
+    };
+    for (int kt = 0; kt < n_tiles; kt += 2) {
+        tile(StageTag<0>{}, kt);
+        if (kt + 1 < n_tiles) tile(StageTag<1>{}, kt + 1);
     }
 
     lsum = pair_sum(lsum);

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
             const float mold = sm.bm[h];
             const float mnew = fmaxf(fmaxf(mold, fmaxf(sm.red[0][h], sm.red[1][h])),
                                      fmaxf(sm.red[2][h], sm.red[3][h]));
-            alpha[h] = exp2f(mold - mnew);  // 0 when mold == -inf
+            alpha[h] = __builtin_amdgcn_exp2f(mold - mnew);  // 0 when mold == -inf
             lacc[h] *= alpha[h];
 #pragma unroll
             for (int i = 0; i < 8; ++i) o[h][i] *= alpha[h];
@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(const DecodeArgs a) {
         __syncthreads();
         // weights, once per (row, head)
         for (int idx = tid; idx < n * R; idx += kThreads)
-            sm.sc[idx] = exp2f(sm.sc[idx] - sm.bm[idx % R]);
+            sm.sc[idx] = __builtin_amdgcn_exp2f(sm.sc[idx] - sm.bm[idx % R]);
         __syncthreads();
         // pass 2: P V
         for (int i0 = wave * RPW + sub; i0 < n; i0 += RPB * UNR) {
