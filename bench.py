@@ -250,7 +250,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--rows", default="all", help="extra hot-path rows: all | none")
+    ap.add_argument("--rows", default="all",
+                    help="extra hot-path rows: all | none | comma list of row names")
     ap.add_argument("--reps", type=int, default=5, help="repetitions per extra row")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -271,17 +272,21 @@ def main():
     traffic = None
     rows = {}
     if args.rows != "none":
+        want = None if args.rows == "all" else set(args.rows.split(","))
+        pick = lambda name: want is None or name in want
         del tensors
         torch.cuda.empty_cache()
         for name, fn in (("a4_prune_gather", lambda: prune_row(dev, args.reps)),
                          ("a6_prefill_config3", lambda: prefill_row(3, dev, args.reps)),
                          ("a6_prefill_config4", lambda: prefill_row(4, dev, args.reps))):
-            log("row", name)
-            rows[name] = fn()
-            log("  ", json.dumps(rows[name]))
-        log("row a7_decode_config5 + a5_route_build")
-        rows["a7_decode_config5"], rows["a5_route_build"] = decode_row(dev, args.reps)
-        log("  ", json.dumps(rows["a7_decode_config5"]))
+            if pick(name):
+                log("row", name)
+                rows[name] = fn()
+                log("  ", json.dumps(rows[name]))
+        if pick("a7_decode_config5") or pick("a5_route_build"):
+            log("row a7_decode_config5 + a5_route_build")
+            rows["a7_decode_config5"], rows["a5_route_build"] = decode_row(dev, args.reps)
+            log("  ", json.dumps(rows["a7_decode_config5"]))
         tensors = w.tensors(dev)
     cpu = None
     if not args.no_cpu_baseline:

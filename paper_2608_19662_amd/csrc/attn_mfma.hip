@@ -199,13 +199,20 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
 
     // ---- K / V tiles in LDS, both row-major [64 keys][HD] with the 16-byte
-    // chunks of each row XOR-swizzled by the key's low bits, double buffered.
+    // chunks of each row XOR-swizzled by the key's low four bits, double
+    // buffered.
     constexpr int ROWB = HD * 2;
     constexpr int TILEB = kBK * ROWB;
     constexpr int STAGEB = 2 * TILEB;  // K tile, then V tile
     char* lds = reinterpret_cast<char*>(sm.kv);
+    // XOR mask of a row's chunk index: for 256-byte rows the two 2-bit halves
+    // of row % 16 are swapped, which keeps the 16 rows of an A-operand read on
+    // 16 distinct chunks and puts the four rows of one transpose-read lane
+    // group on four distinct 4-chunk groups (both bank-conflict free, as
+    // measured with the LDS conflict counter).
     auto swz = [](int row, int chunk) -> uint32_t {
-        return (uint32_t)(row * ROWB + ((chunk ^ (row % TL::CPR)) << 4));
+        const int m = TL::CPR == 16 ? (((row & 3) << 2) | ((row >> 2) & 3)) : (row % TL::CPR);
+        return (uint32_t)(row * ROWB + ((chunk ^ m) << 4));
     };
 
     // Staging: thread owns keys kq*KPT + [0, KPT) at chunk c (coalesced rows).
@@ -237,37 +244,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
 
     u32x4 kreg[TL::KPT], vreg[TL::KPT];
-    auto row_ptr_off = [&](int p, const uint16_t*& kp, const uint16_t*& vp) {
-        p = min(p, stream - 1);
-        if constexpr (ENCODE) {
-            kp = kbase + (size_t)p * HD;
-            vp = vbase + (size_t)p * HD;
-        } else {
-            size_t row;
-            if (p < s_vis) {
-                int lo = 0, hi = n_seg - 1;  // last segment with start <= p
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (sm.seg_start[mid] <= p) lo = mid; else hi = mid - 1;
-                }
-                row = (size_t)(sm.seg_row[lo] + (p - sm.seg_start[lo]));
-                row = min(row, (size_t)a.k_rows - 1);
+    // Prefill streams visit segments in order, so each thread keeps the index
+    // of the segment holding its current row and only ever moves it forward.
+    int sidx = 0;
+    auto load_tile = [&](int kt) {
+        const int p0 = kt * kBK + kq * TL::KPT;
+#pragma unroll
+        for (int j = 0; j < TL::KPT; ++j) {
+            const int p = min(p0 + j, stream - 1);
+            const uint16_t* kp;
+            const uint16_t* vp;
+            if constexpr (ENCODE) {
+                kp = kbase + (size_t)p * HD;
+                vp = vbase + (size_t)p * HD;
+            } else if (p < s_vis) {
+                while (sidx + 1 < n_seg && sm.seg_start[sidx + 1] <= p) ++sidx;
+                const size_t row = min((size_t)(sm.seg_row[sidx] + (p - sm.seg_start[sidx])),
+                                       (size_t)a.k_rows - 1);
                 kp = kbase + row * HD;
                 vp = vbase + row * HD;
             } else {
-                row = (size_t)ctx_row0 + (p - s_vis);
-                row = min(row, (size_t)a.c_rows - 1);
+                const size_t row = min((size_t)ctx_row0 + (p - s_vis), (size_t)a.c_rows - 1);
                 kp = a.ck + ((size_t)g * a.c_rows + row) * HD;
                 vp = a.cv + ((size_t)g * a.c_rows + row) * HD;
             }
-        }
-    };
-    auto load_tile = [&](int kt) {
-#pragma unroll
-        for (int j = 0; j < TL::KPT; ++j) {
-            const uint16_t* kp;
-            const uint16_t* vp;
-            row_ptr_off(kt * kBK + kq * TL::KPT + j, kp, vp);
             kreg[j] = *reinterpret_cast<const u32x4*>(kp + c * 8);
             vreg[j] = *reinterpret_cast<const u32x4*>(vp + c * 8);
         }
@@ -291,6 +291,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
 #pragma unroll
     for (int db = 0; db < TL::NDB; ++db) oacc[db] = f32x16{};
     const int lim = off + my_q;  // keys p <= lim are visible to this lane's row
+    const float lazy = 8.0f / sl2;
+    const bf16x2 ones2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0) in bf16
 
     auto tile = [&](auto stage_tag, int kt) {
         constexpr int cur = decltype(stage_tag)::value;
@@ -308,22 +310,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         }
         // causal / stream-end mask, only on tiles that reach past the first row's limit
         if (kt * kBK + kBK - 1 > off + q_first) {
+            const int rem = lim - kt * kBK - half * 4;  // key offsets above rem are masked
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int p = kt * kBK + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-                    if (p > lim) sacc[kb][r] = -INFINITY;
-                }
+                for (int r = 0; r < 16; ++r)
+                    if (kb * 32 + (r >> 2) * 8 + (r & 3) > rem) sacc[kb][r] = -INFINITY;
         }
-        float mt = sacc[0][0];
+        float mt = fmaxf(sacc[0][0], sacc[0][1]);
 #pragma unroll
-        for (int r = 1; r < 16; ++r) mt = fmaxf(mt, sacc[0][r]);
+        for (int r = 2; r < 16; ++r) mt = fmaxf(mt, sacc[0][r]);
 #pragma unroll
         for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[1][r]);
         mt = pair_max(mt);
-        const float m_new = fmaxf(m, mt);
-        if (__builtin_amdgcn_ballot_w64(m_new > m)) {
+        // Lazy rescale: weights are taken relative to m, which only moves when
+        // a logit exceeds it by more than 8 / sl2 (weights stay <= 2^8, far
+        // from overflow); O and the row sum share m, so the result is exact.
+        if (__builtin_amdgcn_ballot_w64(mt > m + lazy)) {
+            const float m_new = fmaxf(m, mt);
             const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
             lsum *= alpha;
 #pragma unroll
@@ -334,18 +338,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         bf16x8 pf[4];
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            float p[8];
+            uint32_t w[4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + e], sl2, -msl));
-            u32x4 w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                       pack_bf16x2(p[6], p[7])};
-            // normalise by the weights as rounded for the P V product, so that
-            // the output is an exact weighted mean of the V rows it used
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                lsum += __uint_as_float(w[i] << 16) + __uint_as_float(w[i] & 0xffff0000u);
-            pf[s] = __builtin_bit_cast(bf16x8, w);
+            for (int i = 0; i < 4; ++i) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + 2 * i], sl2, -msl));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + 2 * i + 1], sl2, -msl));
+                w[i] = pack_bf16x2(p0, p1);
+                // row sum of the weights as rounded for the P V product, so the
+                // output is an exact weighted mean of the V rows it used
+                lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[i]), ones2, lsum, false);
+            }
+            pf[s] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
         }
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db) {
