@@ -254,6 +254,9 @@ def main():
                     help="extra hot-path rows: all | none | comma list of row names")
     ap.add_argument("--reps", type=int, default=5, help="repetitions per extra row")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain elementwise copy (int32 negation, reads and writes "
+                         "MIB MiB) 5 times: the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -264,6 +267,15 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.neg(src, out=dst)  # an elementwise kernel, not a DMA copy
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
+        return
     log("headline: config 2 encode, %d warmup + %d steps" % (args.warmup, args.steps))
     w, h, tensors = headline(args, dev)
     log("headline done: %.3f ms/step, %.1f TFLOP/s (attention kernel %.3f ms, rope %.3f ms)" % (

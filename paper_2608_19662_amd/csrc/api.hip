@@ -56,8 +56,8 @@ int check_heads(int dtype, int n_q_heads, int n_kv_heads) {
             "n_q_heads %d is not a multiple of n_kv_heads %d", n_q_heads, n_kv_heads);
     const int r = n_q_heads / n_kv_heads;
     if (dtype == RECACHE_BF16)
-        REQUIRE(r == 1 || r == 2 || r == 4 || r == 8, RECACHE_EUNSUPPORTED,
-                "bf16 kernels take 1, 2, 4 or 8 query heads per KV head, not %d", r);
+        REQUIRE(r >= 1 && r <= 8, RECACHE_EUNSUPPORTED,
+                "bf16 kernels take 1 to 8 query heads per KV head, not %d", r);
     return RECACHE_OK;
 }
 
@@ -154,6 +154,16 @@ int check_encode(int dtype, int n_res, const int32_t* cu_len, int total_T, int m
     return RECACHE_OK;
 }
 
+// MFMA attention tiling: a block covers 4 (query head, 32-row block) pairs of
+// one KV group, as hpw heads x rbw row blocks with hpw the largest of 4, 2, 1
+// dividing the group size (so every head of the group is covered exactly once).
+void set_tiling(AttnArgs& a, int ratio, int max_rows) {
+    a.hpw = ratio % 4 == 0 ? 4 : ratio % 2 == 0 ? 2 : 1;
+    a.rbw = 4 / a.hpw;
+    a.n_hq = ratio / a.hpw;
+    a.n_qt = (max_rows + 32 * a.rbw - 1) / (32 * a.rbw);
+}
+
 hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, int total_T,
                                    int max_len, int n_q_heads, int n_kv_heads, int head_dim,
                                    const RopeRev& rope, const int32_t* pos_base,
@@ -166,11 +176,8 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
         a.n_q_heads = n_q_heads;
         a.n_kv_heads = n_kv_heads;
         a.ratio = ratio;
-        a.hpw = ratio < 4 ? ratio : 4;
-        a.rbw = 4 / a.hpw;
-        a.n_hq = ratio / a.hpw;
+        set_tiling(a, ratio, max_len);
         a.n_units = n_res;
-        a.n_qt = (max_len + 32 * a.rbw - 1) / (32 * a.rbw);
         a.scale_log2 = scale * 1.4426950408889634f;
         a.q = static_cast<const uint16_t*>(q);
         a.out = static_cast<uint16_t*>(out);
@@ -408,11 +415,8 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
     a.n_q_heads = n_q_heads;
     a.n_kv_heads = n_kv_heads;
     a.ratio = ratio;
-    a.hpw = ratio < 4 ? ratio : 4;
-    a.rbw = 4 / a.hpw;
-    a.n_hq = ratio / a.hpw;
+    set_tiling(a, ratio, max_q);
     a.n_units = n_req;
-    a.n_qt = (max_q + 32 * a.rbw - 1) / (32 * a.rbw);
     a.scale_log2 = scale * 1.4426950408889634f;
     a.q = static_cast<const uint16_t*>(q);
     a.out = static_cast<uint16_t*>(out);

@@ -11,15 +11,20 @@
 // off = 0.  Prefill: unit = request, stream = [routed kept rows in request
 // order] ++ [context rows], off = S_vis + Tc - Tq.
 //
-// Work decomposition.  A workgroup is 4 waves that share one KV group: it
-// holds up to 4 query heads of the group over 32 query rows (or fewer heads
-// over 64 / 128 rows when the group has fewer heads).  Each wave owns one
-// (head, 32-row block) and computes the transposed products
+// Work decomposition.  A workgroup is 4 waves that share one KV group and
+// 4 * P (query head, 32-row block) pairs of it (hpw heads x rbw row blocks,
+// hpw the largest of 4, 2, 1 dividing the group size).  Each wave owns P pairs
+// and computes, for each, the transposed products
 //     S^T = K Q^T    (32x32x16 bf16 MFMA; A = K rows from LDS, B = Q^T in VGPRs)
 //     O^T += V^T P^T (A = V^T from LDS, B = P^T straight from the S^T accumulators)
-// so every lane owns exactly one query row in both accumulators: row max and
-// row sum need one cross-lane step (lanes l and l^32), and the rescale of O is
-// lane-local.  K / V tiles of 64 keys are staged through LDS, double buffered
+// Every A fragment read from LDS feeds the MFMAs of all P pairs.  P = 2 halves
+// LDS traffic per flop but needs ~500 registers per lane, so only one wave
+// fits per SIMD and the softmax of one wave can no longer hide behind another
+// wave's MFMAs; on MI355X it measured slower than P = 1 at two waves per SIMD
+// (encode 0.35 vs 0.47 PFLOP/s), so the launcher instantiates P = 1.  Each
+// lane owns exactly one query row of a pair in both accumulators, so row max
+// and row sum need one cross-lane step (lanes l and l^32) and the rescale of O
+// is lane-local.  K / V tiles of 64 keys are staged through LDS, double buffered
 // (global loads of tile t+1 are in flight while tile t is computed).  Both
 // tiles are stored row-major with an XOR swizzle of their 16-byte chunks; the
 // V^T operand is read with gfx950's LDS transpose reads, in the key order in
@@ -38,13 +43,14 @@ namespace {
 constexpr int kBK = 64;  // keys per tile
 constexpr int kThreads = 256;
 
-template <int HD>
+template <int HD, int P>
 struct Tile {
     static constexpr int CPR = HD / 8;              // 16-byte chunks per row
     static constexpr int KPT = kBK * CPR / kThreads;  // keys per thread per tile (4 or 2)
     static constexpr int NT = HD / 16;              // MFMA k-steps over head_dim
     static constexpr int NDB = HD / 32;             // 32-wide blocks of head_dim
     static constexpr int STAGE = 2 * kBK * HD;      // bf16 elements per stage (K + V)
+    static constexpr int ROPE = 128 * P * HD * 2;   // bf16-sized elements of a cos/sin table for 128 * P rows
 };
 
 constexpr int kMaxSeg = 1024;
@@ -54,24 +60,28 @@ struct StageTag {
     static constexpr int value = C;
 };
 
-template <int HD, bool ENCODE>
+template <int HD, bool ENCODE, int P>
 struct Smem {
-    uint16_t kv[2 * Tile<HD>::STAGE];
+    // encode also stages a cos / sin table for up to 128 * P query rows here
+    alignas(16) uint16_t kv[(ENCODE && Tile<HD, P>::ROPE > 2 * Tile<HD, P>::STAGE)
+                                ? Tile<HD, P>::ROPE
+                                : 2 * Tile<HD, P>::STAGE];
     int seg_start[ENCODE ? 1 : kMaxSeg + 1];
     int seg_row[ENCODE ? 1 : kMaxSeg];
     int scan[ENCODE ? 1 : kThreads];
 };
 
-template <int HD, bool ENCODE>
-__global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a) {
-    using TL = Tile<HD>;
-    __shared__ Smem<HD, ENCODE> sm;
+template <int HD, bool ENCODE, int P>
+__global__ __launch_bounds__(kThreads, P == 1 ? 2 : 1) void attn_mfma_kernel(const AttnArgs a) {
+    using TL = Tile<HD, P>;
+    constexpr int kPairs = P;
+    __shared__ Smem<HD, ENCODE, P> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, half = lane >> 5;
 
-    // block -> (q tile [longest first], unit, head quarter, group); the group
+    // block -> (q tile [longest first], unit, head slice, group); the group
     // is the fastest index so that one group's blocks share an XCD's L2.
     int bid = blockIdx.x;
     const int g = bid % a.n_kv_heads;
@@ -150,52 +160,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
     const int n_tiles = (off + q_last) / kBK + 1;
 
-    const int hpw = a.hpw;
-    const int head = g * a.ratio + hq * hpw + (wave % hpw);
-    const int my_q = q_first + (wave / hpw) * 32 + l32;
-    // rows outside [0, lse_rows) of q / out are never touched
-    const int my_q_c = max(0, min(min(my_q, q_len - 1), (int)a.lse_rows - 1 - q_row0));
-    const bool store = my_q < q_len && q_row0 + my_q < a.lse_rows;
-
-    // ---- Q fragment (B operand of S^T = K Q^T): lane holds row my_q, elements
-    // d = t*16 + half*8 + [0,8) for t < NT.
-    bf16x8 qf[TL::NT];
-    {
-        const uint16_t* qrow = a.q + ((size_t)(q_row0 + my_q_c) * a.n_q_heads + head) * HD;
-        u32x4 raw[TL::NT];
+    // The (head, row block) pairs of this wave.
+    int head[kPairs], my_q[kPairs], my_q_c[kPairs];
+    bool store[kPairs];
 #pragma unroll
-        for (int t = 0; t < TL::NT; ++t)
-            raw[t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
-        if constexpr (ENCODE) {
-            // RoPE at the resource-local position, pairs (f, f + HD/2) are
-            // (t, t + NT/2) in this lane.
-            const int pos = pos0 + my_q_c;
-#pragma unroll
-            for (int t = 0; t < TL::NT / 2; ++t) {
-                uint32_t lo[4], hi[4];
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    float y1[2], y2[2];
-#pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2) {
-                        const int f = t * 16 + half * 8 + w * 2 + h2;
-                        float s, c;
-                        sincos_rev_fast(rope_revolutions(pos, a.rope.rev[f]), &s, &c);
-                        const float x1 = bf16_bits_to_f32((raw[t][w] >> (16 * h2)) & 0xffffu);
-                        const float x2 =
-                            bf16_bits_to_f32((raw[t + TL::NT / 2][w] >> (16 * h2)) & 0xffffu);
-                        y1[h2] = x1 * c - x2 * s;
-                        y2[h2] = x2 * c + x1 * s;
-                    }
-                    lo[w] = pack_bf16x2(y1[0], y1[1]);
-                    hi[w] = pack_bf16x2(y2[0], y2[1]);
-                }
-                raw[t] = u32x4{lo[0], lo[1], lo[2], lo[3]};
-                raw[t + TL::NT / 2] = u32x4{hi[0], hi[1], hi[2], hi[3]};
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < TL::NT; ++t) qf[t] = __builtin_bit_cast(bf16x8, raw[t]);
+    for (int j = 0; j < kPairs; ++j) {
+        const int u = wave * kPairs + j;
+        head[j] = g * a.ratio + hq * a.hpw + u % a.hpw;
+        my_q[j] = q_first + (u / a.hpw) * 32 + l32;
+        // rows outside [0, lse_rows) of q / out are never touched
+        my_q_c[j] = max(0, min(min(my_q[j], q_len - 1), (int)a.lse_rows - 1 - q_row0));
+        store[j] = my_q[j] < q_len && q_row0 + my_q[j] < a.lse_rows;
     }
 
     // ---- K / V tiles in LDS, both row-major [64 keys][HD] with the 16-byte
@@ -280,75 +255,158 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         }
     };
 
+    // Issue the first tile's loads, then the query loads, so that their
+    // latencies overlap (and overlap the RoPE table set-up in encode).
     load_tile(0);
+
+    // ---- Q fragments (B operand of S^T = K Q^T): for pair j the lane holds
+    // row my_q[j], elements d = t*16 + half*8 + [0,8) for t < NT.
+    bf16x8 qf[kPairs][TL::NT];
+    {
+        u32x4 raw[kPairs][TL::NT];
+#pragma unroll
+        for (int j = 0; j < kPairs; ++j) {
+            const uint16_t* qrow = a.q + ((size_t)(q_row0 + my_q_c[j]) * a.n_q_heads + head[j]) * HD;
+#pragma unroll
+            for (int t = 0; t < TL::NT; ++t)
+                raw[j][t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
+        }
+        if constexpr (ENCODE) {
+            // RoPE at the resource-local position.  cos / sin for the block's
+            // rows are computed once into LDS (in the tile buffers, before the
+            // first tile arrives): row r, frequency f sits in 16-byte chunk
+            // (f / 2) ^ (r % 16) of the row, so the 16 rows read by a lane
+            // group fall on distinct banks.  Pairs (f, f + HD/2) are
+            // (t, t + NT/2) in this lane.
+            constexpr int HALF = HD / 2;
+            char* tab = reinterpret_cast<char*>(sm.kv);
+            for (int idx = tid; idx < wg_rows * HALF; idx += kThreads) {
+                const int r = idx / HALF, f = idx % HALF;
+                float sn, cs;
+                sincos_rev_fast(rope_revolutions(pos0 + min(q_first + r, q_len - 1), a.rope.rev[f]),
+                                &sn, &cs);
+                *reinterpret_cast<float2*>(tab + r * (HALF * 8) + (((f >> 1) ^ (r & 15)) << 4) +
+                                           (f & 1) * 8) = make_float2(cs, sn);
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kPairs; ++j) {
+                const int r = my_q[j] - q_first;
+                const char* trow = tab + r * (HALF * 8);
+#pragma unroll
+                for (int t = 0; t < TL::NT / 2; ++t) {
+                    uint32_t lo[4], hi[4];
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const int f = t * 16 + half * 8 + w * 2;  // even: one chunk holds f, f + 1
+                        const f32x4 k = *reinterpret_cast<const f32x4*>(trow + (((f >> 1) ^ (r & 15)) << 4));
+                        float y1[2], y2[2];
+#pragma unroll
+                        for (int h2 = 0; h2 < 2; ++h2) {
+                            const float cs = k[2 * h2], sn = k[2 * h2 + 1];
+                            const float x1 = bf16_bits_to_f32((raw[j][t][w] >> (16 * h2)) & 0xffffu);
+                            const float x2 =
+                                bf16_bits_to_f32((raw[j][t + TL::NT / 2][w] >> (16 * h2)) & 0xffffu);
+                            y1[h2] = x1 * cs - x2 * sn;
+                            y2[h2] = x2 * cs + x1 * sn;
+                        }
+                        lo[w] = pack_bf16x2(y1[0], y1[1]);
+                        hi[w] = pack_bf16x2(y2[0], y2[1]);
+                    }
+                    raw[j][t] = u32x4{lo[0], lo[1], lo[2], lo[3]};
+                    raw[j][t + TL::NT / 2] = u32x4{hi[0], hi[1], hi[2], hi[3]};
+                }
+            }
+            __syncthreads();  // the table area is reused by the first tile
+        }
+#pragma unroll
+        for (int j = 0; j < kPairs; ++j)
+#pragma unroll
+            for (int t = 0; t < TL::NT; ++t) qf[j][t] = __builtin_bit_cast(bf16x8, raw[j][t]);
+    }
     store_tile(lds);
     __syncthreads();
 
     const float sl2 = a.scale_log2;
-    float m = -INFINITY;  // running max of raw logits for this lane's row
-    float lsum = 0.f;     // this lane's partial sum of the (bf16-rounded) weights
-    f32x16 oacc[TL::NDB];
-#pragma unroll
-    for (int db = 0; db < TL::NDB; ++db) oacc[db] = f32x16{};
-    const int lim = off + my_q;  // keys p <= lim are visible to this lane's row
     const float lazy = 8.0f / sl2;
     const bf16x2 ones2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0) in bf16
+    float m[kPairs], lsum[kPairs];
+    int lim[kPairs];
+    f32x16 oacc[kPairs][TL::NDB];
+#pragma unroll
+    for (int j = 0; j < kPairs; ++j) {
+        m[j] = -INFINITY;  // running max of raw logits for this lane's row
+        lsum[j] = 0.f;     // this lane's partial sum of the (bf16-rounded) weights
+        lim[j] = off + my_q[j];  // keys p <= lim are visible to this lane's row
+#pragma unroll
+        for (int db = 0; db < TL::NDB; ++db) oacc[j][db] = f32x16{};
+    }
 
     auto tile = [&](auto stage_tag, int kt) {
         constexpr int cur = decltype(stage_tag)::value;
         const char* st = lds + cur * STAGEB;
         if (kt + 1 < n_tiles) load_tile(kt + 1);
 
-        f32x16 sacc[2] = {f32x16{}, f32x16{}};
+        f32x16 sacc[kPairs][2];
+#pragma unroll
+        for (int j = 0; j < kPairs; ++j) sacc[j][0] = sacc[j][1] = f32x16{};
 #pragma unroll
         for (int t = 0; t < TL::NT; ++t) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 const bf16x8 av = *reinterpret_cast<const bf16x8*>(st + k_rd[t] + kb * 32 * ROWB);
-                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[t], sacc[kb], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < kPairs; ++j)
+                    sacc[j][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[j][t], sacc[j][kb], 0, 0, 0);
             }
         }
-        // causal / stream-end mask, only on tiles that reach past the first row's limit
-        if (kt * kBK + kBK - 1 > off + q_first) {
-            const int rem = lim - kt * kBK - half * 4;  // key offsets above rem are masked
+        const bool diag = kt * kBK + kBK - 1 > off + q_first;
+        bf16x8 pf[kPairs][4];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+        for (int j = 0; j < kPairs; ++j) {
+            // causal / stream-end mask, only on tiles that reach past the first row's limit
+            if (diag) {
+                const int rem = lim[j] - kt * kBK - half * 4;  // key offsets above rem are masked
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (kb * 32 + (r >> 2) * 8 + (r & 3) > rem) sacc[kb][r] = -INFINITY;
-        }
-        float mt = fmaxf(sacc[0][0], sacc[0][1]);
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 2; r < 16; ++r) mt = fmaxf(mt, sacc[0][r]);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[1][r]);
-        mt = pair_max(mt);
-        // Lazy rescale: weights are taken relative to m, which only moves when
-        // a logit exceeds it by more than 8 / sl2 (weights stay <= 2^8, far
-        // from overflow); O and the row sum share m, so the result is exact.
-        if (__builtin_amdgcn_ballot_w64(mt > m + lazy)) {
-            const float m_new = fmaxf(m, mt);
-            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
-            lsum *= alpha;
-#pragma unroll
-            for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
-            m = m_new;
-        }
-        const float msl = m * sl2;
-        bf16x8 pf[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            uint32_t w[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + 2 * i], sl2, -msl));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[s >> 1][8 * (s & 1) + 2 * i + 1], sl2, -msl));
-                w[i] = pack_bf16x2(p0, p1);
-                // row sum of the weights as rounded for the P V product, so the
-                // output is an exact weighted mean of the V rows it used
-                lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[i]), ones2, lsum, false);
+                    for (int r = 0; r < 16; ++r)
+                        if (kb * 32 + (r >> 2) * 8 + (r & 3) > rem) sacc[j][kb][r] = -INFINITY;
             }
-            pf[s] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+            float mt = fmaxf(sacc[j][0][0], sacc[j][0][1]);
+#pragma unroll
+            for (int r = 2; r < 16; ++r) mt = fmaxf(mt, sacc[j][0][r]);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[j][1][r]);
+            mt = pair_max(mt);
+            // Lazy rescale: weights are taken relative to m, which only moves
+            // when a logit exceeds it by more than 8 / sl2 (weights stay <=
+            // 2^8, far from overflow); O and the row sum share m, so the
+            // result is exact.
+            if (__builtin_amdgcn_ballot_w64(mt > m[j] + lazy)) {
+                const float m_new = fmaxf(m[j], mt);
+                const float alpha = __builtin_amdgcn_exp2f((m[j] - m_new) * sl2);  // 0 when m == -inf
+                lsum[j] *= alpha;
+#pragma unroll
+                for (int db = 0; db < TL::NDB; ++db) oacc[j][db] *= alpha;
+                m[j] = m_new;
+            }
+            const float msl = m[j] * sl2;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                uint32_t w[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[j][s >> 1][8 * (s & 1) + 2 * i], sl2, -msl));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[j][s >> 1][8 * (s & 1) + 2 * i + 1], sl2, -msl));
+                    w[i] = pack_bf16x2(p0, p1);
+                    // row sum of the weights as rounded for the P V product, so
+                    // the output is an exact weighted mean of the V rows it used
+                    lsum[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[i]), ones2,
+                                                              lsum[j], false);
+                }
+                pf[j][s] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+            }
         }
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db) {
@@ -361,7 +419,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                     (lds_s16x4*)(st + v_rd[db][1] + s * 16 * ROWB));
                 const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
                 const bf16x8 av = __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
-                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pf[s], oacc[db], 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < kPairs; ++j)
+                    oacc[j][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pf[j][s], oacc[j][db], 0, 0, 0);
             }
         }
         if (kt + 1 < n_tiles) store_tile(lds + (cur ^ 1) * STAGEB);
@@ -372,22 +432,25 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         if (kt + 1 < n_tiles) tile(StageTag<1>{}, kt + 1);
     }
 
-    lsum = pair_sum(lsum);
-    if (store) {
-        const float inv = 1.0f / lsum;
-        uint16_t* orow = a.out + ((size_t)(q_row0 + my_q) * a.n_q_heads + head) * HD;
 #pragma unroll
-        for (int db = 0; db < TL::NDB; ++db)
+    for (int j = 0; j < kPairs; ++j) {
+        const float l = pair_sum(lsum[j]);
+        if (store[j]) {
+            const float inv = 1.0f / l;
+            uint16_t* orow = a.out + ((size_t)(q_row0 + my_q[j]) * a.n_q_heads + head[j]) * HD;
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const int d = db * 32 + r4 * 8 + half * 4;
-                const uint2 w = make_uint2(pack_bf16x2(oacc[db][r4 * 4 + 0] * inv, oacc[db][r4 * 4 + 1] * inv),
-                                           pack_bf16x2(oacc[db][r4 * 4 + 2] * inv, oacc[db][r4 * 4 + 3] * inv));
-                *reinterpret_cast<uint2*>(orow + d) = w;
-            }
-        if (a.lse && half == 0)
-            a.lse[(size_t)head * a.lse_rows + q_row0 + my_q] =
-                m * sl2 * 0.69314718055994531f + logf(lsum);
+            for (int db = 0; db < TL::NDB; ++db)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const int d = db * 32 + r4 * 8 + half * 4;
+                    const uint2 w = make_uint2(pack_bf16x2(oacc[j][db][r4 * 4 + 0] * inv, oacc[j][db][r4 * 4 + 1] * inv),
+                                               pack_bf16x2(oacc[j][db][r4 * 4 + 2] * inv, oacc[j][db][r4 * 4 + 3] * inv));
+                    *reinterpret_cast<uint2*>(orow + d) = w;
+                }
+            if (a.lse && half == 0)
+                a.lse[(size_t)head[j] * a.lse_rows + q_row0 + my_q[j]] =
+                    m[j] * sl2 * 0.69314718055994531f + logf(l);
+        }
     }
 }
 
@@ -397,13 +460,14 @@ hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStr
     const long blocks = (long)a.n_qt * a.n_units * a.n_hq * a.n_kv_heads;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    if (a.hpw * a.rbw != 4) return hipErrorInvalidValue;  // one pair per wave
     dim3 grid((unsigned)blocks), block(kThreads);
     if (head_dim == 128) {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, a);
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true, 1>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((attn_mfma_kernel<128, false, 1>), grid, block, 0, stream, a);
     } else {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, a);
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true, 1>), grid, block, 0, stream, a);
+        else hipLaunchKernelGGL((attn_mfma_kernel<64, false, 1>), grid, block, 0, stream, a);
     }
     return hipGetLastError();
 }

@@ -52,17 +52,20 @@ __device__ __forceinline__ float dot8_bf16(const u32x4& k, const u32x4& q, float
     return acc;
 }
 
-// One row's R logits into LDS with a single vector store.
+// One row's R logits into LDS with as few vector stores as alignment allows.
 template <int R>
 __device__ __forceinline__ void store_row(float* dst, const float* v) {
-    if constexpr (R == 1) {
-        dst[0] = v[0];
-    } else if constexpr (R == 2) {
-        *reinterpret_cast<float2*>(dst) = make_float2(v[0], v[1]);
-    } else {
+    // dst = sc + i * R is 16-byte aligned when R % 4 == 0, 8-byte when R is even
+    if constexpr (R % 4 == 0) {
 #pragma unroll
         for (int j = 0; j < R; j += 4)
             *reinterpret_cast<float4*>(dst + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+    } else if constexpr (R % 2 == 0) {
+#pragma unroll
+        for (int j = 0; j < R; j += 2) *reinterpret_cast<float2*>(dst + j) = make_float2(v[j], v[j + 1]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < R; ++j) dst[j] = v[j];
     }
 }
 
@@ -355,15 +358,27 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t s) {
     if ((long)a.n_req * a.n_kv_heads * a.n_splits > 0x7fffffffL) return hipErrorInvalidValue;
     const int R = a.ratio;
     if (a.head_dim == 128) {
-        if (R == 1) return launch_dec<128, 1>(a, s);
-        if (R == 2) return launch_dec<128, 2>(a, s);
-        if (R == 4) return launch_dec<128, 4>(a, s);
-        if (R == 8) return launch_dec<128, 8>(a, s);
+        switch (R) {
+            case 1: return launch_dec<128, 1>(a, s);
+            case 2: return launch_dec<128, 2>(a, s);
+            case 3: return launch_dec<128, 3>(a, s);
+            case 4: return launch_dec<128, 4>(a, s);
+            case 5: return launch_dec<128, 5>(a, s);
+            case 6: return launch_dec<128, 6>(a, s);
+            case 7: return launch_dec<128, 7>(a, s);
+            case 8: return launch_dec<128, 8>(a, s);
+        }
     } else {
-        if (R == 1) return launch_dec<64, 1>(a, s);
-        if (R == 2) return launch_dec<64, 2>(a, s);
-        if (R == 4) return launch_dec<64, 4>(a, s);
-        if (R == 8) return launch_dec<64, 8>(a, s);
+        switch (R) {
+            case 1: return launch_dec<64, 1>(a, s);
+            case 2: return launch_dec<64, 2>(a, s);
+            case 3: return launch_dec<64, 3>(a, s);
+            case 4: return launch_dec<64, 4>(a, s);
+            case 5: return launch_dec<64, 5>(a, s);
+            case 6: return launch_dec<64, 6>(a, s);
+            case 7: return launch_dec<64, 7>(a, s);
+            case 8: return launch_dec<64, 8>(a, s);
+        }
     }
     return hipErrorInvalidValue;
 }

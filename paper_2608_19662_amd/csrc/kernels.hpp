@@ -14,8 +14,8 @@ namespace rc {
 struct AttnArgs {
     // decomposition: blocks = n_qt * n_units * n_hq * n_kv_heads
     int n_q_heads, n_kv_heads, ratio;
-    int hpw;      // query heads per block (min(ratio, 4))
-    int rbw;      // 32-row blocks per block (4 / hpw)
+    int hpw;      // query heads per block (largest of 4, 2, 1 dividing ratio)
+    int rbw;      // 32-row blocks per block (4 / hpw: one (head, row block) pair per wave)
     int n_hq;     // blocks per group along heads (ratio / hpw)
     int n_units;  // resources (encode) or requests (prefill)
     int n_qt;     // query tiles per unit (ceil(max rows / (32 * rbw)))

@@ -66,7 +66,7 @@ def enc(**kw):
     (dict(d=96), rc.EUNSUPPORTED),
     (dict(dtype=2), rc.EUNSUPPORTED),
     (dict(Hq=30), rc.EINVAL),
-    (dict(Hq=24), rc.EUNSUPPORTED),  # 3 query heads per KV head on the bf16 kernels
+    (dict(Hq=72), rc.EUNSUPPORTED),  # 9 query heads per KV head on the bf16 kernels
     (dict(n_res=0), rc.EINVAL),
     (dict(total_T=1), rc.EINVAL),
     (dict(max_len=0), rc.EINVAL),
@@ -82,8 +82,8 @@ def test_encode_rejects(kw, code):
 
 
 def test_encode_fp32_any_ratio_passes_head_check():
-    # fp32 path accepts 3 query heads per KV head; the next check (null q) still fires
-    assert enc(dtype=0, Hq=24, q=None) == rc.EINVAL
+    # fp32 path accepts 9 query heads per KV head; the next check (null q) still fires
+    assert enc(dtype=0, Hq=72, q=None) == rc.EINVAL
     assert "null" in rc.last_error()
 
 

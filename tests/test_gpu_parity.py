@@ -85,7 +85,8 @@ ENC_LENGTHS = [1, 2, 31, 32, 33, 63, 64, 65, 97, 128, 129, 200]
 
 
 @pytest.mark.parametrize("Hq,Hkv,d", [(32, 8, 128), (8, 2, 64), (8, 8, 128), (16, 8, 128),
-                                      (64, 8, 128), (16, 2, 64)])
+                                      (64, 8, 128), (16, 2, 64), (28, 4, 128), (12, 4, 64),
+                                      (24, 4, 128)])
 def test_encode_bf16_ragged(Hq, Hkv, d):
     print_case("encode ragged", Hq, Hkv, d)
     w = EncodeWorkload(seed=11, lengths=np.array(ENC_LENGTHS, np.int32), n_q_heads=Hq,
@@ -284,6 +285,8 @@ PREFILL_CASES = [
     (23, 4, 8, 16, 8, 128, [65, 2, 31, 128], [65, 40, 31, 300]),
     (24, 2, 4, 64, 8, 128, [40, 90], [41, 90]),
     (25, 2, 4, 8, 8, 128, [129, 5], [129, 300]),
+    (26, 2, 5, 28, 4, 128, [70, 300], [80, 300]),
+    (27, 2, 4, 24, 4, 64, [33, 260], [40, 270]),
 ]
 
 
@@ -316,6 +319,8 @@ DECODE_CASES = [
     (43, 4, 10, 64, 8, 128, [1] * 4, [100, 2000, 1, 513]),
     (44, 2, 4, 8, 8, 128, [1, 1], [250, 7]),
     (45, 3, 30, 16, 8, 128, [1] * 3, [3000, 5, 800]),
+    (46, 3, 6, 28, 4, 128, [1] * 3, [900, 3, 129]),
+    (47, 2, 5, 12, 4, 64, [1] * 2, [400, 64]),
 ]
 
 
