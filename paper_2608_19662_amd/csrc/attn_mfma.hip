@@ -34,12 +34,24 @@
 // Tiles never cross a resource boundary in encode, and the reduction order
 // depends only on local indices, so a resource's outputs are bit-identical
 // wherever it is packed and whatever its neighbours are.
+#include <utility>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace rc {
 
 namespace {
+
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 constexpr int kBK = 64;  // keys per tile
 constexpr int kThreads = 256;
@@ -59,6 +71,13 @@ struct Tile {
     static constexpr int NT = HD / 16;           // MFMA k-steps over head_dim
     static constexpr int NDB = HD / 32;          // 32-wide blocks of head_dim
 };
+
+// Small per-lane index sets live in vector registers rather than arrays, so
+// that selecting between two of them never turns into a stack access.
+template <int N>
+using u32v = uint32_t __attribute__((ext_vector_type(N)));
+template <int N>
+using u64v = uint64_t __attribute__((ext_vector_type(N)));
 
 template <int C>
 struct StageTag {
@@ -191,59 +210,126 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     const int cp_lane_row = lane / TL::CPR;
     const int cp_chunk0 = (lane % TL::CPR) ^ chunk_mask<TL::CPR>(wave * 16 + cp_lane_row);
     auto cp_chunk = [&](int j) { return TL::CPR == 16 ? (cp_chunk0 ^ j) : cp_chunk0; };
-    // This lane's keys of one tile: element offsets from the group's K / V
-    // base (encode), or K addresses plus a context flag per key (prefill).
-    uint32_t koff[TL::NJ];
-    const uint16_t* kp[TL::NJ];
+    // Where one tile comes from.  A "fast" tile lies inside one segment, or
+    // inside the context, or (encode) inside the resource: its 64 rows are
+    // consecutive, so each copy reads a wave-uniform base plus a per-lane
+    // constant, with no per-lane address arithmetic.  Tiles that straddle a
+    // boundary or the end of the stream take per-lane addresses: element
+    // offsets from the group's K / V base (encode), or K addresses plus a
+    // context flag per key (prefill).
+    u32v<TL::NJ> lane_off;  // this lane's element offset within a run of 64 rows
+#pragma unroll
+    for (int j = 0; j < TL::NJ; ++j)
+        lane_off[j] = (uint32_t)(wave * 16 + j * TL::RPI + cp_lane_row) * HD + cp_chunk(j) * 8;
+    bool t_fast = false;  // wave-uniform
+    const uint16_t* t_kb = a.k;
+    const uint16_t* t_vb = a.v;
+    u32v<TL::NJ> koff = {};
+    u64v<TL::NJ> kp = {};
     uint32_t in_ctx = 0;
     const uint16_t* kgrp = a.k + ((size_t)g * a.k_rows + q_row0) * HD;  // encode only
     const uint16_t* vgrp = a.v + ((size_t)g * a.k_rows + q_row0) * HD;
-    // Prefill streams visit segments in order, so each lane keeps the segment
-    // holding its current key in registers and only moves it forward.
+    // Prefill streams visit segments in order.  The wave keeps the segment of
+    // its current tile's first key (for the fast test), and each lane the
+    // segment of its current key (for straddling tiles); both only move forward.
+    int u_sidx = 0, u_hi = 0, u_dl = 0;
     int sidx = 0, seg_hi = 0, seg_dl = 0;
     if constexpr (!ENCODE) {
         if (n_seg > 0) {
-            seg_hi = sm.seg_start[1];
-            seg_dl = sm.seg_row[0];
+            u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[1]);
+            u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[0]);
+            seg_hi = u_hi;
+            seg_dl = u_dl;
         }
     }
     auto key_ptrs = [&](int kt) {
-#pragma unroll
-        for (int j = 0; j < TL::NJ; ++j) {
-            const int p = min(kt * kBK + wave * 16 + j * TL::RPI + cp_lane_row, stream - 1);
-            if constexpr (ENCODE) {
-                koff[j] = (uint32_t)p * HD + cp_chunk(j) * 8;
-            } else if (p < s_vis) {
-                while (p >= seg_hi && sidx + 1 < n_seg) {
-                    ++sidx;
-                    seg_hi = sm.seg_start[sidx + 1];
-                    seg_dl = sm.seg_row[sidx] - sm.seg_start[sidx];
-                }
-                const size_t row = min((size_t)(seg_dl + p), (size_t)a.k_rows - 1);
-                kp[j] = a.k + ((size_t)g * a.k_rows + row) * HD + cp_chunk(j) * 8;
-                in_ctx &= ~(1u << j);
+        const int p0 = kt * kBK;
+        if constexpr (ENCODE) {
+            t_fast = p0 + kBK <= stream;
+            if (t_fast) {
+                t_kb = kgrp + (size_t)p0 * HD;
+                t_vb = vgrp + (size_t)p0 * HD;
             } else {
-                const size_t row = min((size_t)ctx_row0 + (p - s_vis), (size_t)a.c_rows - 1);
-                kp[j] = a.ck + ((size_t)g * a.c_rows + row) * HD + cp_chunk(j) * 8;
-                in_ctx |= 1u << j;
+                static_for<TL::NJ>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    const int p = min(p0 + wave * 16 + j * TL::RPI + cp_lane_row, stream - 1);
+                    koff[j] = (uint32_t)p * HD + cp_chunk(j) * 8;
+                });
+            }
+        } else {
+            t_fast = false;
+            if (p0 + kBK <= s_vis) {
+                while (p0 >= u_hi && u_sidx + 1 < n_seg) {
+                    ++u_sidx;
+                    u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx + 1]);
+                    u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[u_sidx]) -
+                           __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx]);
+                }
+                const long row0 = (long)u_dl + p0;
+                if (p0 + kBK <= u_hi && row0 >= 0 && row0 + kBK <= a.k_rows) {
+                    t_fast = true;
+                    t_kb = a.k + ((size_t)g * a.k_rows + row0) * HD;
+                    t_vb = a.v + ((size_t)g * a.k_rows + row0) * HD;
+                }
+            } else if (p0 >= s_vis && p0 + kBK <= stream) {
+                const long row0 = (long)ctx_row0 + (p0 - s_vis);
+                if (row0 + kBK <= a.c_rows) {
+                    t_fast = true;
+                    t_kb = a.ck + ((size_t)g * a.c_rows + row0) * HD;
+                    t_vb = a.cv + ((size_t)g * a.c_rows + row0) * HD;
+                }
+            }
+            if (!t_fast) {
+                static_for<TL::NJ>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    const int p = min(p0 + wave * 16 + j * TL::RPI + cp_lane_row, stream - 1);
+                    if (p < s_vis) {
+                        while (p >= seg_hi && sidx + 1 < n_seg) {
+                            ++sidx;
+                            seg_hi = sm.seg_start[sidx + 1];
+                            seg_dl = sm.seg_row[sidx] - sm.seg_start[sidx];
+                        }
+                        const size_t row = min((size_t)(seg_dl + p), (size_t)a.k_rows - 1);
+                        kp[j] = (uint64_t)(a.k + ((size_t)g * a.k_rows + row) * HD + cp_chunk(j) * 8);
+                        in_ctx &= ~(1u << j);
+                    } else {
+                        const size_t row = min((size_t)ctx_row0 + (p - s_vis), (size_t)a.c_rows - 1);
+                        kp[j] = (uint64_t)(a.ck + ((size_t)g * a.c_rows + row) * HD + cp_chunk(j) * 8);
+                        in_ctx |= 1u << j;
+                    }
+                });
             }
         }
     };
     // the same element of V: the two buffers share their layout
     const ptrdiff_t v_res = a.v - a.k, v_ctx = a.cv - a.ck;
     auto copy = [&](bool is_v, int dst_byte) {
-#pragma unroll
-        for (int j = 0; j < TL::NJ; ++j) {
-            const uint16_t* src;
-            if constexpr (ENCODE) src = (is_v ? vgrp : kgrp) + koff[j];
-            else src = is_v ? kp[j] + ((in_ctx >> j) & 1 ? v_ctx : v_res) : kp[j];
-            __builtin_amdgcn_global_load_lds(
-                src, (lds_void*)(lds + dst_byte + (wave * 16 + j * TL::RPI) * ROWB), 16, 0, 0);
+        char* dst = lds + dst_byte + wave * 16 * ROWB;
+        // Per-copy addresses first, then one sequence of copies: the two
+        // paths only differ in how the addresses are formed.
+        u64v<TL::NJ> src;
+        if (t_fast) {
+            const uint16_t* base = is_v ? t_vb : t_kb;
+            static_for<TL::NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                src[j] = (uint64_t)(base + lane_off[j]);
+            });
+        } else {
+            static_for<TL::NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                if constexpr (ENCODE) src[j] = (uint64_t)((is_v ? vgrp : kgrp) + koff[j]);
+                else src[j] = is_v ? kp[j] + 2 * ((in_ctx >> j) & 1 ? v_ctx : v_res) : kp[j];
+            });
         }
+        static_for<TL::NJ>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            __builtin_amdgcn_global_load_lds((const void*)src[j], (lds_void*)(dst + j * TL::RPI * ROWB), 16,
+                                             0, 0);
+        });
     };
 
     // Prologue copies: K(0), V(0) into stage 0, K(1) into stage 1.  The
-    // addresses of tile 1 are kept for V(1) in the first loop iteration.
+    // sources of tile 1 are kept for V(1) in the first loop iteration.
     key_ptrs(0);
     copy(false, 0);
     copy(true, TILEB);
