@@ -123,15 +123,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     const int lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, half = lane >> 5;
 
-    // block -> (q tile [longest first], unit, head slice, group); the group
-    // is the fastest index so that one group's blocks share an XCD's L2.
+    // block -> (unit, head slice, q tile [longest first], group).  The group
+    // is the fastest index, so the blocks of one group land on one XCD, and
+    // the q tiles of a (unit, group) come next, so the blocks that run side
+    // by side on an XCD stream the same keys through its L2.
     int bid = blockIdx.x;
     const int g = bid % a.n_kv_heads;
     bid /= a.n_kv_heads;
+    const int jt = a.n_qt - 1 - bid % a.n_qt;
+    bid /= a.n_qt;
     const int hq = bid % a.n_hq;
-    bid /= a.n_hq;
-    const int unit = bid % a.n_units;
-    const int jt = a.n_qt - 1 - bid / a.n_units;
+    const int unit = bid / a.n_hq;
 
     int q_len, q_row0, off, stream, pos0 = 0;
     int n_seg = 0, s_vis = 0, ctx_row0 = 0, tc = 0;
