@@ -330,8 +330,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         });
     };
 
-    // Prologue copies: K(0), V(0) into stage 0, K(1) into stage 1.  The
+    // Query rows first (they are needed first, for the RoPE), then the
+    // prologue copies: K(0), V(0) into stage 0, K(1) into stage 1.  The
     // sources of tile 1 are kept for V(1) in the first loop iteration.
+    u32x4 qraw[TL::NT];
+    {
+        const uint16_t* qrow = a.q + ((size_t)(q_row0 + my_q_c) * a.n_q_heads + head) * HD;
+#pragma unroll
+        for (int t = 0; t < TL::NT; ++t)
+            qraw[t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
+    }
     key_ptrs(0);
     copy(false, 0);
     copy(true, TILEB);
@@ -344,11 +352,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     // d = t*16 + half*8 + [0,8) for t < NT.
     bf16x8 qf[TL::NT];
     {
-        const uint16_t* qrow = a.q + ((size_t)(q_row0 + my_q_c) * a.n_q_heads + head) * HD;
-        u32x4 raw[TL::NT];
-#pragma unroll
-        for (int t = 0; t < TL::NT; ++t)
-            raw[t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
+        u32x4* raw = qraw;
         if constexpr (ENCODE) {
             // RoPE at the resource-local position; the pairs (f, f + HD/2) are
             // (t, t + NT/2) in this lane.  For blocks of 32 rows (4 heads) the
