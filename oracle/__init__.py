@@ -123,15 +123,25 @@ def rope(x, pos, base: float, rot_dtype=None) -> np.ndarray:
 
 
 def encode(q, k, v, cu_len, base: float, scale: float | None = None, pos_base=None,
-           rot_dtype=None):
+           rot_dtype=None, prefix_k=None, prefix_v=None):
     """Block-diagonal causal encode of packed resources (one layer).
 
     q[T][Hq][d], k/v[T][Hkv][d] in stored precision.  Rotated queries and keys
     are rounded to the precision of rot_dtype (default: the inputs' dtype).
+    An optional shared prefix is given as its rotated cache prefix_k/prefix_v
+    [Hkv][P][d] in the inputs' dtype; every resource row attends all of it.
     Returns a dict of float64 arrays: out[T][Hq][d], k_cache/v_cache[Hkv][T][d],
     lse[Hq][T].
     """
     q, k, v = host_view(q), host_view(k), host_view(v)
+    if (prefix_k is None) != (prefix_v is None):
+        raise ValueError("prefix_k and prefix_v go together")
+    p_len = 0
+    if prefix_k is not None:
+        prefix_k, prefix_v = host_view(prefix_k), host_view(prefix_v)
+        if prefix_k.dtype != q.dtype or prefix_v.dtype != q.dtype:
+            raise ValueError("the prefix cache has the inputs' dtype")
+        p_len = prefix_k.shape[1]
     cu_len = _i32(cu_len)
     pos_base = _i32(pos_base)
     T, Hq, d = q.shape
@@ -147,6 +157,7 @@ def encode(q, k, v, cu_len, base: float, scale: float | None = None, pos_base=No
         ctypes.c_int(_dtype_code(q)), ctypes.c_int(len(cu_len) - 1), _p(cu_len),
         ctypes.c_int(Hq), ctypes.c_int(Hkv), ctypes.c_int(d), ctypes.c_double(base),
         _p(pos_base), ctypes.c_double(scale), _p(q), _p(k), _p(v),
+        ctypes.c_int(p_len), _p(prefix_k), _p(prefix_v),
         _p(out), _p(kc), _p(vc), _p(lse), ctypes.c_int(_rot(q, rot_dtype)))
     _check(rc, "encode")
     return {"out": out, "k_cache": kc, "v_cache": vc, "lse": lse}

@@ -144,8 +144,13 @@ static double softmax_average(const double* z, int n, int d, vrow_fn vrow, void*
  * Resources are packed in order: resource r owns rows [cu_len[r], cu_len[r+1])
  * of q[T][Hq][d], k[T][Hkv][d], v[T][Hkv][d].  Token j of resource r sits at
  * position pos_base[r] + j (pos_base == NULL means 0: resource-local).
- * Query row t of resource r, head h, attends keys u in [cu_len[r], t] of KV
- * head h / (Hq / Hkv), with logits scale * <RoPE(q_t), RoPE(k_u)>.
+ * Query row t of resource r, head h, attends every row of the shared prefix
+ * (if any) and keys u in [cu_len[r], t] of KV head h / (Hq / Hkv), with
+ * logits scale * <RoPE(q_t), RoPE(k_u)>.  The shared prefix is the part of
+ * the input every resource is encoded after (Sec. 3: resource tokens attend
+ * the shared prefix and their local resource tokens); it is given as its
+ * already rotated cache, prefix_k / prefix_v [Hkv][prefix_len][d] in the
+ * input dtype, used as stored.
  *
  * Rotated queries and keys are rounded to the precision of rot_dtype (the
  * workload's storage dtype; fp64 keeps them exact).
@@ -153,20 +158,29 @@ static double softmax_average(const double* z, int n, int d, vrow_fn vrow, void*
  * Outputs (double): out[T][Hq][d]; k_cache[Hkv][T][d] holds the rotated keys
  * and v_cache[Hkv][T][d] the values (head-major); lse[Hq][T] (optional)
  * holds the natural-log sum-exp of the scaled logits.                      */
-struct enc_vctx { const double* vc; int T, d, g, row0; };
+struct enc_vctx {
+    const double* vc; int T, d, g, row0;
+    const void* pv; int p_len, dtype;
+};
 static const double* enc_vrow(void* c, int u, double* scratch) {
-    (void)scratch;
     struct enc_vctx* x = (struct enc_vctx*)c;
-    return x->vc + ((size_t)x->g * x->T + x->row0 + u) * x->d;
+    if (u < x->p_len) {  /* prefix row u */
+        for (int e = 0; e < x->d; ++e)
+            scratch[e] = widen(x->pv, x->dtype, ((size_t)x->g * x->p_len + u) * x->d + e);
+        return scratch;
+    }
+    return x->vc + ((size_t)x->g * x->T + x->row0 + (u - x->p_len)) * x->d;
 }
 
 int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, int d,
                   double base, const int32_t* pos_base, double scale,
                   const void* q, const void* k, const void* v,
+                  int prefix_len, const void* prefix_k, const void* prefix_v,
                   double* out, double* k_cache, double* v_cache, double* lse, int rot_dtype) {
     if (n_res <= 0 || !cu_len || Hq <= 0 || Hkv <= 0 || Hq % Hkv || d <= 0 || d > 512 ||
         (d % 2) || !q || !k || !v || !out || !k_cache || !v_cache)
         return -1;
+    if (prefix_len < 0 || (prefix_len > 0 && (!prefix_k || !prefix_v))) return -1;
     if (cu_len[0] != 0) return -1;
     int max_len = 0;
     for (int r = 0; r < n_res; ++r) {
@@ -195,8 +209,8 @@ int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, 
 
 #pragma omp parallel
     {
-        double* z = (double*)malloc(sizeof(double) * (size_t)max_len);
-        double qv[512], qr[512];
+        double* z = (double*)malloc(sizeof(double) * ((size_t)prefix_len + max_len));
+        double qv[512], qr[512], kv[512], vs[512];
 #pragma omp for schedule(dynamic, 16)
         for (long th = 0; th < (long)T * Hq; ++th) {
             int t = (int)(th / Hq), h = (int)(th % Hq), g = h / ratio;
@@ -207,14 +221,23 @@ int oracle_encode(int dtype, int n_res, const int32_t* cu_len, int Hq, int Hkv, 
             for (int e = 0; e < d; ++e) qv[e] = widen(q, dtype, ((size_t)t * Hq + h) * d + e);
             oracle_rope_vec(qv, qr, d, base, p);
             for (int e = 0; e < d; ++e) qr[e] = round_to(qr[e], rot_dtype);
+            /* keys: the prefix rows, then rows o .. o + j of the resource */
+            for (int u = 0; u < prefix_len; ++u) {
+                for (int e = 0; e < d; ++e)
+                    kv[e] = widen(prefix_k, dtype, ((size_t)g * prefix_len + u) * d + e);
+                double dot = 0.0;
+                for (int e = 0; e < d; ++e) dot += qr[e] * kv[e];
+                z[u] = scale * dot;
+            }
             for (int u = 0; u <= j; ++u) {
                 const double* kr = k_cache + ((size_t)g * T + o + u) * d;
                 double dot = 0.0;
                 for (int e = 0; e < d; ++e) dot += qr[e] * kr[e];
-                z[u] = scale * dot;
+                z[prefix_len + u] = scale * dot;
             }
-            struct enc_vctx c = {v_cache, T, d, g, o};
-            double l = softmax_average(z, j + 1, d, enc_vrow, &c, out + (size_t)th * d, NULL);
+            struct enc_vctx c = {v_cache, T, d, g, o, prefix_v, prefix_len, dtype};
+            double l = softmax_average(z, prefix_len + j + 1, d, enc_vrow, &c,
+                                       out + (size_t)th * d, vs);
             if (lse) lse[(size_t)h * T + t] = l;
         }
         free(z);

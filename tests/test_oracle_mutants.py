@@ -28,8 +28,14 @@ MUTANTS = {
                               "double p = (double)((pos_base ? pos_base[r] : 0) + t);"),
     "encode_drops_diagonal": ("for (int u = 0; u <= j; ++u) {",
                               "for (int u = 0; u <= j - (j > 0); ++u) {"),
-    "scale_dropped_encode": ("z[u] = scale * dot;\n            }\n            struct enc_vctx",
-                             "z[u] = dot;\n            }\n            struct enc_vctx"),
+    "scale_dropped_encode": ("z[prefix_len + u] = scale * dot;",
+                             "z[prefix_len + u] = dot;"),
+    "prefix_scale_dropped": ("z[u] = scale * dot;\n            }\n            for (int u = 0; u <= j; ++u) {",
+                             "z[u] = dot;\n            }\n            for (int u = 0; u <= j; ++u) {"),
+    "prefix_not_visible": ("z[u] = scale * dot;\n            }\n            for (int u = 0; u <= j; ++u) {",
+                           "z[u] = -INFINITY;\n            }\n            for (int u = 0; u <= j; ++u) {"),
+    "prefix_v_row_shifted": ("return x->vc + ((size_t)x->g * x->T + x->row0 + (u - x->p_len)) * x->d;",
+                             "return x->vc + ((size_t)x->g * x->T + x->row0 + u) * x->d;"),
     "scale_dropped_attend": ("z[u] = scale * dot;\n            }\n            struct att_vctx",
                              "z[u] = dot;\n            }\n            struct att_vctx"),
     "gqa_modulo": ("int s = (int)(sh / Hq), h = (int)(sh % Hq), g = h / ratio;",
@@ -66,6 +72,8 @@ PINS = [
     pins.test_encode_blockdiag_matches_bruteforce_and_lse,
     pins.test_encode_first_token_is_its_value_row,
     pins.test_encode_zero_queries_give_running_mean,
+    lambda: pins.test_encode_with_prefix_is_causal_attention_over_prefix_then_resource(False),
+    lambda: pins.test_encode_with_prefix_is_causal_attention_over_prefix_then_resource(True),
     lambda: pins.test_attend_matches_bruteforce_final_mask(3),
     lambda: pins.test_attend_matches_bruteforce_final_mask(4),
     pins.test_attend_all_ones_mask_is_causal_over_concatenation,

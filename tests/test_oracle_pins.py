@@ -165,6 +165,50 @@ def test_encode_bf16_storage_precision_matches_bruteforce():
     assert np.array_equal(enc["k_cache"], head_major(kr))
 
 
+def _prefix_case(seed, lengths, P, Hq, Hkv, d):
+    rng = np.random.default_rng(seed)
+    T = int(sum(lengths))
+    q, k, v = (rng.standard_normal((T, h, d)) for h in (Hq, Hkv, Hkv))
+    pq, pk, pv = (rng.standard_normal((P, h, d)) for h in (Hq, Hkv, Hkv))
+    return q, k, v, pq, pk, pv, np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+
+
+@pytest.mark.parametrize("block_positions", [False, True])
+def test_encode_with_prefix_is_causal_attention_over_prefix_then_resource(block_positions):
+    """Sec. 3: resource tokens attend the shared prefix and their own tokens.
+    For each resource, its rows must equal rows P.. of textbook causal
+    attention over the sequence [prefix, that resource]; positions are 0..P-1
+    for the prefix and pos_base[r] + j for the resource (pos_base = P, or the
+    original global positions P + cu_len[r] for the "Block" variant)."""
+    lengths, P, Hq, Hkv, d, base = [9, 1, 14, 6], 11, 4, 2, 16, 1e4
+    q, k, v, pq, pk, pv, cu = _prefix_case(5, lengths, P, Hq, Hkv, d)
+    pos_base = (P + cu[:-1] if block_positions else np.full(len(lengths), P)).astype(np.int32)
+    pkr = bf.rope_complex(pk, np.arange(P), base)  # the cached, already rotated prefix keys
+    enc = oracle.encode(q, k, v, cu, base, pos_base=pos_base,
+                        prefix_k=np.ascontiguousarray(head_major(pkr)),
+                        prefix_v=np.ascontiguousarray(head_major(pv)))
+    for r, D in enumerate(lengths):
+        sl = slice(cu[r], cu[r + 1])
+        pos = np.concatenate([np.arange(P), pos_base[r] + np.arange(D)])
+        qq = bf.rope_complex(np.concatenate([pq, q[sl]]), pos, base)
+        kk = bf.rope_complex(np.concatenate([pk, k[sl]]), pos, base)
+        ref = sdpa_causal(qq, kk, np.concatenate([pv, v[sl]]), 1 / np.sqrt(d), Hq // Hkv)
+        assert np.max(np.abs(enc["out"][sl] - ref[P:])) < 1e-12
+    # the cache rows of the resources are unaffected by the prefix
+    plain = oracle.encode(q, k, v, cu, base, pos_base=pos_base)
+    assert np.array_equal(enc["k_cache"], plain["k_cache"])
+    assert np.array_equal(enc["v_cache"], plain["v_cache"])
+
+
+def test_encode_empty_prefix_is_no_prefix():
+    lengths, Hq, Hkv, d = [5, 8], 4, 2, 8
+    q, k, v, _, _, _, cu = _prefix_case(6, lengths, 0, Hq, Hkv, d)
+    empty = np.zeros((Hkv, 0, d))
+    a = oracle.encode(q, k, v, cu, 1e4, prefix_k=empty, prefix_v=empty)
+    b = oracle.encode(q, k, v, cu, 1e4)
+    assert np.array_equal(a["out"], b["out"]) and np.array_equal(a["lse"], b["lse"])
+
+
 def test_encode_first_token_is_its_value_row():
     t = make_tiny(3, n_res=7, d=8)
     enc = oracle.encode(t.q, t.k, t.v, t.cu_len, t.base)
