@@ -257,6 +257,34 @@ def measured_traffic():
     return float(fields["traffic_bytes_per_launch"])
 
 
+def prefix_encode_row(dev, reps, P=512):
+    """Config 2's resources encoded after a shared P-token prefix (resource
+    positions start at P): the attention kernel alone, prefix cache resident."""
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config, normal
+
+    w = config(2)["encode"]
+    T, Hq, Hkv, d = w.total, w.n_q_heads, w.n_kv_heads, w.head_dim
+    q, k, v = w.tensors(dev)
+    cu = i32(w.cu_len, dev)
+    pb = i32(np.full(len(w.lengths), P), dev)
+    kc = torch.empty(Hkv, T, d, dtype=q.dtype, device=dev)
+    vc = torch.empty_like(kc)
+    rc.rope_kv(k, v, i32(np.concatenate([P + np.arange(n) for n in w.lengths]), dev), w.rope_base,
+               kc, vc)
+    pk = normal((Hkv, P, d), q.dtype, 2, 40, dev)
+    pv = normal((Hkv, P, d), q.dtype, 2, 41, dev)
+    out = torch.empty_like(q)
+    L = w.lengths.astype(np.int64)
+    flops = 4.0 * d * Hq * float(np.sum(L * (L + 1) // 2 + P * L))
+    ms = timed(lambda: rc.encode_attention(q, kc, vc, cu, int(L.max()), w.rope_base, out,
+                                           pos_base=pb, prefix_k=pk, prefix_v=pv), reps)
+    return {"workload": "config 2 after a shared %d-token prefix" % P, "ms": ms,
+            "tflops": flops / (ms * 1e-3) / 1e12, "flops": flops,
+            "pct_of_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+
 def cpu_baseline(w, tensors, min_seconds=10.0, max_passes=10):
     """The fp64 oracle on the headline workload: whole passes over all 16
     resources, repeated until about min_seconds of CPU time have been spent."""
@@ -320,6 +348,7 @@ def main():
         del tensors
         torch.cuda.empty_cache()
         for name, fn in (("a4_prune_gather", lambda: prune_row(dev, args.reps)),
+                         ("f1_encode_prefix_config2", lambda: prefix_encode_row(dev, args.reps)),
                          ("a6_prefill_config3", lambda: prefill_row(3, dev, args.reps)),
                          ("a6_prefill_config4", lambda: prefill_row(4, dev, args.reps))):
             if pick(name):

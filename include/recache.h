@@ -104,20 +104,30 @@ int recache_rope_kv(int dtype, int T, int n_kv_heads, int head_dim, double rope_
  * gets position pos_base[r] + j (pos_base device int32 [n_res], or NULL for
  * 0: resource-local positions, pos(t_ij) = j).
  *
- * Query row t of resource r, head h, attends keys u in [cu_len[r], t] of KV
- * head h / (Hq / Hkv) only: no attention crosses resources, so each
- * resource's outputs and cache rows do not depend on its neighbours or on
- * its packing offset (bit-exact on the GPU).
+ * Optional shared prefix (the instruction every resource is encoded after,
+ * Sec. 3: resource tokens attend the shared prefix and their own tokens):
+ * prefix_len rows of an already rotated cache, prefix_k/prefix_v
+ * [n_kv_heads][prefix_len][head_dim] (device; NULL when prefix_len is 0).
+ * With a prefix, pos_base[r] = prefix_len places every resource right after
+ * it; pos_base[r] = prefix_len + (tokens before r) gives the original global
+ * positions ("Block").
+ *
+ * Query row t of resource r, head h, attends every prefix row and keys u in
+ * [cu_len[r], t] of KV head h / (Hq / Hkv): no attention crosses resources,
+ * so each resource's outputs and cache rows do not depend on its neighbours
+ * or on its packing offset (bit-exact on the GPU).
  *
  *   q[total_T][n_q_heads][head_dim], k/v[total_T][n_kv_heads][head_dim]: inputs
  *   out[total_T][n_q_heads][head_dim]: attention output
  *   k_cache/v_cache[n_kv_heads][total_T][head_dim]: rotated K and plain V,
  *       the resource KV blocks to keep for reuse
  *   lse[n_q_heads][total_T] (fp32) or NULL
+ * Errors: RECACHE_EINVAL also for prefix_len < 0 or a missing prefix pointer.
  */
 int recache_encode_resources(int dtype, int n_res, const int32_t* cu_len, int total_T,
                              int max_len, int n_q_heads, int n_kv_heads, int head_dim,
-                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             double rope_base, const int32_t* pos_base, int prefix_len,
+                             const void* prefix_k, const void* prefix_v, float softmax_scale,
                              const void* q, const void* k, const void* v, void* out,
                              void* k_cache, void* v_cache, float* lse, void* stream);
 
@@ -131,7 +141,8 @@ int recache_encode_resources(int dtype, int n_res, const int32_t* cu_len, int to
  */
 int recache_encode_attention(int dtype, int n_res, const int32_t* cu_len, int total_T,
                              int max_len, int n_q_heads, int n_kv_heads, int head_dim,
-                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             double rope_base, const int32_t* pos_base, int prefix_len,
+                             const void* prefix_k, const void* prefix_v, float softmax_scale,
                              const void* q, const void* k_cache, const void* v_cache, void* out,
                              float* lse, void* stream);
 

@@ -139,7 +139,8 @@ int recache_rope_kv(int dtype, int T, int n_kv_heads, int head_dim, double rope_
 namespace {
 
 int check_encode(int dtype, int n_res, const int32_t* cu_len, int total_T, int max_len,
-                 int n_q_heads, int n_kv_heads, int head_dim, double rope_base, float softmax_scale) {
+                 int n_q_heads, int n_kv_heads, int head_dim, double rope_base, float softmax_scale,
+                 int prefix_len, const void* prefix_k, const void* prefix_v) {
     int rc_ = check_dtype_dim(dtype, head_dim);
     if (rc_) return rc_;
     if ((rc_ = check_heads(dtype, n_q_heads, n_kv_heads))) return rc_;
@@ -151,6 +152,9 @@ int check_encode(int dtype, int n_res, const int32_t* cu_len, int total_T, int m
             max_len, total_T);
     REQUIRE(cu_len, RECACHE_EINVAL, "null pointer argument");
     REQUIRE(!(isnan(softmax_scale) || isinf(softmax_scale)), RECACHE_EINVAL, "softmax_scale not finite");
+    REQUIRE(prefix_len >= 0, RECACHE_EINVAL, "prefix_len %d must be >= 0", prefix_len);
+    REQUIRE(prefix_len == 0 || (prefix_k && prefix_v), RECACHE_EINVAL,
+            "prefix_len %d needs prefix_k and prefix_v", prefix_len);
     return RECACHE_OK;
 }
 
@@ -166,7 +170,8 @@ void set_tiling(AttnArgs& a, int ratio, int max_rows) {
 
 hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, int total_T,
                                    int max_len, int n_q_heads, int n_kv_heads, int head_dim,
-                                   const RopeRev& rope, const int32_t* pos_base,
+                                   const RopeRev& rope, const int32_t* pos_base, int prefix_len,
+                                   const void* prefix_k, const void* prefix_v,
                                    float softmax_scale, const void* q, const void* k_cache,
                                    const void* v_cache, void* out, float* lse, hipStream_t s) {
     const float scale = resolve_scale(softmax_scale, head_dim);
@@ -183,9 +188,14 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
         a.out = static_cast<uint16_t*>(out);
         a.lse = lse;
         a.lse_rows = total_T;
-        a.k = static_cast<const uint16_t*>(k_cache);
-        a.v = static_cast<const uint16_t*>(v_cache);
-        a.k_rows = total_T;
+        // segments: the shared prefix; causal part: the resources' own rows
+        a.k = static_cast<const uint16_t*>(prefix_k);
+        a.v = static_cast<const uint16_t*>(prefix_v);
+        a.k_rows = prefix_len;
+        a.ck = static_cast<const uint16_t*>(k_cache);
+        a.cv = static_cast<const uint16_t*>(v_cache);
+        a.c_rows = total_T;
+        a.p_len = prefix_len;
         a.cu_len = cu_len;
         a.pos_base = pos_base;
         a.rope = rope;
@@ -203,9 +213,13 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
     a.out = static_cast<float*>(out);
     a.lse = lse;
     a.lse_rows = total_T;
-    a.k = static_cast<const float*>(k_cache);
-    a.v = static_cast<const float*>(v_cache);
-    a.k_rows = total_T;
+    a.k = static_cast<const float*>(prefix_k);
+    a.v = static_cast<const float*>(prefix_v);
+    a.k_rows = prefix_len;
+    a.ck = static_cast<const float*>(k_cache);
+    a.cv = static_cast<const float*>(v_cache);
+    a.c_rows = total_T;
+    a.p_len = prefix_len;
     a.cu_len = cu_len;
     a.pos_base = pos_base;
     a.rope = rope;
@@ -216,11 +230,12 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
 
 int recache_encode_resources(int dtype, int n_res, const int32_t* cu_len, int total_T,
                              int max_len, int n_q_heads, int n_kv_heads, int head_dim,
-                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             double rope_base, const int32_t* pos_base, int prefix_len,
+                             const void* prefix_k, const void* prefix_v, float softmax_scale,
                              const void* q, const void* k, const void* v, void* out,
                              void* k_cache, void* v_cache, float* lse, void* stream) {
     int rc_ = check_encode(dtype, n_res, cu_len, total_T, max_len, n_q_heads, n_kv_heads, head_dim,
-                           rope_base, softmax_scale);
+                           rope_base, softmax_scale, prefix_len, prefix_k, prefix_v);
     if (rc_) return rc_;
     REQUIRE(q && k && v && out && k_cache && v_cache, RECACHE_EINVAL, "null pointer argument");
     const hipStream_t s = as_stream(stream);
@@ -245,25 +260,27 @@ int recache_encode_resources(int dtype, int n_res, const int32_t* cu_len, int to
     hipError_t e = launch_rope(ra, s);
     if (e != hipSuccess) return hip_status(e, "encode: rope/cache launch");
     e = encode_attention_launch(dtype, n_res, cu_len, total_T, max_len, n_q_heads, n_kv_heads,
-                                head_dim, ra.rope, pos_base, softmax_scale, q, k_cache, v_cache,
-                                out, lse, s);
+                                head_dim, ra.rope, pos_base, prefix_len, prefix_k, prefix_v,
+                                softmax_scale, q, k_cache, v_cache, out, lse, s);
     return hip_status(e, "encode: attention launch");
 }
 
 int recache_encode_attention(int dtype, int n_res, const int32_t* cu_len, int total_T,
                              int max_len, int n_q_heads, int n_kv_heads, int head_dim,
-                             double rope_base, const int32_t* pos_base, float softmax_scale,
+                             double rope_base, const int32_t* pos_base, int prefix_len,
+                             const void* prefix_k, const void* prefix_v, float softmax_scale,
                              const void* q, const void* k_cache, const void* v_cache, void* out,
                              float* lse, void* stream) {
     int rc_ = check_encode(dtype, n_res, cu_len, total_T, max_len, n_q_heads, n_kv_heads, head_dim,
-                           rope_base, softmax_scale);
+                           rope_base, softmax_scale, prefix_len, prefix_k, prefix_v);
     if (rc_) return rc_;
     REQUIRE(q && k_cache && v_cache && out, RECACHE_EINVAL, "null pointer argument");
     (void)hipGetLastError();
     return hip_status(encode_attention_launch(dtype, n_res, cu_len, total_T, max_len, n_q_heads,
                                               n_kv_heads, head_dim, make_rope(rope_base, head_dim),
-                                              pos_base, softmax_scale, q, k_cache, v_cache, out,
-                                              lse, as_stream(stream)),
+                                              pos_base, prefix_len, prefix_k, prefix_v,
+                                              softmax_scale, q, k_cache, v_cache, out, lse,
+                                              as_stream(stream)),
                       "encode attention launch");
 }
 

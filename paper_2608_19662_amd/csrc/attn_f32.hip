@@ -6,8 +6,8 @@
 // throughput path.
 //
 // Visibility follows the same definitions as the bf16 kernels: encode rows
-// see their own resource causally (ReCache Sec. 3, "Resource-Wise
-// Attention"); conversation rows see the kept rows of their routed resources
+// see the shared prefix and their own resource causally (ReCache Sec. 3,
+// "Resource-Wise Attention"); conversation rows see the kept rows of their routed resources
 // in request order and then the context causally, bottom-right aligned
 // (Fig. 2, final mask).
 #include "common.hpp"
@@ -82,8 +82,12 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const AttnF32Args a) {
     };
 
     if constexpr (ENCODE) {
-        const float* kb = a.k + ((size_t)g * a.k_rows + q_row0) * d;
-        const float* vb = a.v + ((size_t)g * a.k_rows + q_row0) * d;
+        // the shared prefix, fully visible, then the resource's own rows
+        const float* pk = a.k + (size_t)g * a.k_rows * d;
+        const float* pv = a.v + (size_t)g * a.k_rows * d;
+        for (int u = 0; u < a.p_len; ++u) visit(pk + (size_t)u * d, pv + (size_t)u * d);
+        const float* kb = a.ck + ((size_t)g * a.c_rows + q_row0) * d;
+        const float* vb = a.cv + ((size_t)g * a.c_rows + q_row0) * d;
         for (int u = 0; u <= row; ++u) visit(kb + (size_t)u * d, vb + (size_t)u * d);
     } else {
         const size_t e = ((size_t)unit * a.n_layers + a.layer) * a.n_kv_heads + g;

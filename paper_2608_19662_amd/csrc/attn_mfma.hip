@@ -7,9 +7,12 @@
 //     Fig. 2; Sec. 3, "Structural Pruning" / "Semantic Pruning").
 //
 // Both are one "key stream" per (unit, KV group): a query with local index i
-// sees stream keys p <= off + i.  Encode: unit = resource, stream = its rows,
-// off = 0.  Prefill: unit = request, stream = [routed kept rows in request
-// order] ++ [context rows], off = S_vis + Tc - Tq.
+// sees stream keys p <= off + i.  Encode: unit = resource, stream = [shared
+// prefix rows, fully visible (Sec. 3: resource tokens see the shared prefix
+// and their own tokens)] ++ [its own rows], off = P.  Prefill: unit =
+// request, stream = [routed kept rows in request order] ++ [context rows],
+// off = S_vis + Tc - Tq.  Both are a list of segments followed by a causal
+// part, and share one code path.
 //
 // Work decomposition.  A workgroup is 4 waves that share one KV group and
 // four (query head, 32-row block) pairs of it (hpw heads x rbw row blocks,
@@ -87,8 +90,8 @@ struct StageTag {
 template <int HD, bool ENCODE>
 struct Smem {
     alignas(16) char kv[2 * Tile<HD>::STAGEB];
-    int seg_start[ENCODE ? 1 : kMaxSeg + 1];
-    int seg_row[ENCODE ? 1 : kMaxSeg];
+    int seg_start[ENCODE ? 2 : kMaxSeg + 1];
+    int seg_row[ENCODE ? 2 : kMaxSeg];
     int scan[ENCODE ? 1 : kThreads];
 };
 
@@ -141,9 +144,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         const int o = a.cu_len[unit];
         q_len = a.cu_len[unit + 1] - o;
         q_row0 = o;
-        off = 0;
-        stream = q_len;
         pos0 = a.pos_base ? a.pos_base[unit] : 0;
+        // Keys: the shared prefix (one fully visible segment, rows [0, P) of
+        // the prefix cache in k / v), then the resource's own rows (in ck / cv).
+        s_vis = a.p_len;
+        n_seg = s_vis > 0 ? 1 : 0;
+        ctx_row0 = o;
+        tc = q_len;
     } else {
         q_row0 = a.cu_q[unit];
         q_len = a.cu_q[unit + 1] - q_row0;
@@ -192,10 +199,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         }
         s_vis = sm.scan[kThreads - 1];
         if (tid == 0) sm.seg_start[n_seg] = s_vis;
-        off = s_vis + tc - q_len;
-        stream = s_vis + tc;
         __syncthreads();
     }
+    off = s_vis + tc - q_len;
+    stream = s_vis + tc;
     const int n_tiles = (off + q_last) / kBK + 1;
 
     const int head = g * a.ratio + hq * a.hpw + (wave % a.hpw);
@@ -212,13 +219,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     const int cp_lane_row = lane / TL::CPR;
     const int cp_chunk0 = (lane % TL::CPR) ^ chunk_mask<TL::CPR>(wave * 16 + cp_lane_row);
     auto cp_chunk = [&](int j) { return TL::CPR == 16 ? (cp_chunk0 ^ j) : cp_chunk0; };
-    // Where one tile comes from.  A "fast" tile lies inside one segment, or
-    // inside the context, or (encode) inside the resource: its 64 rows are
-    // consecutive, so each copy reads a wave-uniform base plus a per-lane
-    // constant, with no per-lane address arithmetic.  Tiles that straddle a
-    // boundary or the end of the stream take per-lane addresses: element
-    // offsets from the group's K / V base (encode), or K addresses plus a
-    // context flag per key (prefill).
+    // Where one tile comes from.  A "fast" tile lies inside one segment (the
+    // prefix, in encode) or inside the context (the resource's own rows, in
+    // encode): its 64 rows are consecutive, so each copy reads a wave-uniform
+    // base plus a per-lane constant, with no per-lane address arithmetic.
+    // Tiles that straddle a boundary or the end of the stream take per-lane
+    // addresses: K addresses plus a flag per key for the buffer it is in.
     u32v<TL::NJ> lane_off;  // this lane's element offset within a run of 64 rows
 #pragma unroll
     for (int j = 0; j < TL::NJ; ++j)
@@ -226,39 +232,26 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     bool t_fast = false;  // wave-uniform
     const uint16_t* t_kb = a.k;
     const uint16_t* t_vb = a.v;
-    u32v<TL::NJ> koff = {};
     u64v<TL::NJ> kp = {};
     uint32_t in_ctx = 0;
-    const uint16_t* kgrp = a.k + ((size_t)g * a.k_rows + q_row0) * HD;  // encode only
-    const uint16_t* vgrp = a.v + ((size_t)g * a.k_rows + q_row0) * HD;
-    // Prefill streams visit segments in order.  The wave keeps the segment of
-    // its current tile's first key (for the fast test), and each lane the
-    // segment of its current key (for straddling tiles); both only move forward.
+    // Streams visit segments in order.  The wave keeps the segment of its
+    // current tile's first key (for the fast test), and each lane the segment
+    // of its current key (for straddling tiles); both only move forward.
     int u_sidx = 0, u_hi = 0, u_dl = 0;
     int sidx = 0, seg_hi = 0, seg_dl = 0;
-    if constexpr (!ENCODE) {
-        if (n_seg > 0) {
+    if (n_seg > 0) {
+        if constexpr (ENCODE) {
+            u_hi = s_vis;  // the prefix: stream keys [0, P) are its rows [0, P)
+        } else {
             u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[1]);
             u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[0]);
-            seg_hi = u_hi;
-            seg_dl = u_dl;
         }
+        seg_hi = u_hi;
+        seg_dl = u_dl;
     }
     auto key_ptrs = [&](int kt) {
         const int p0 = kt * kBK;
-        if constexpr (ENCODE) {
-            t_fast = p0 + kBK <= stream;
-            if (t_fast) {
-                t_kb = kgrp + (size_t)p0 * HD;
-                t_vb = vgrp + (size_t)p0 * HD;
-            } else {
-                static_for<TL::NJ>([&](auto jc) {
-                    constexpr int j = decltype(jc)::value;
-                    const int p = min(p0 + wave * 16 + j * TL::RPI + cp_lane_row, stream - 1);
-                    koff[j] = (uint32_t)p * HD + cp_chunk(j) * 8;
-                });
-            }
-        } else {
+        {
             t_fast = false;
             if (p0 + kBK <= s_vis) {
                 while (p0 >= u_hi && u_sidx + 1 < n_seg) {
@@ -319,8 +312,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         } else {
             static_for<TL::NJ>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
-                if constexpr (ENCODE) src[j] = (uint64_t)((is_v ? vgrp : kgrp) + koff[j]);
-                else src[j] = is_v ? kp[j] + 2 * ((in_ctx >> j) & 1 ? v_ctx : v_res) : kp[j];
+                src[j] = is_v ? kp[j] + 2 * ((in_ctx >> j) & 1 ? v_ctx : v_res) : kp[j];
             });
         }
         static_for<TL::NJ>([&](auto jc) {

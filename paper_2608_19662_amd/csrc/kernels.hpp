@@ -24,19 +24,23 @@ struct AttnArgs {
     uint16_t* out;
     float* lse;
     long lse_rows;      // rows of q / out / lse (total_T or total_q); bounds every row index
-    const uint16_t* k;  // encode: rotated K cache; prefill: kept resource rows
+    // Segments (encode: the shared prefix cache, rows [0, p_len); prefill:
+    // kept resource rows) and the causal part (encode: the resources' rotated
+    // K / V caches; prefill: conversation context), all [n_kv_heads][rows][d].
+    const uint16_t* k;
     const uint16_t* v;
     long k_rows;        // rows per KV head in k / v
+    const uint16_t* ck;
+    const uint16_t* cv;
+    long c_rows;        // rows per KV head in ck / cv
     // encode
     const int32_t* cu_len;
     const int32_t* pos_base;
+    int p_len;          // shared prefix rows (0: none)
     RopeRev rope;
     // prefill
     const int32_t* cu_q;
     const int32_t* cu_ctx;
-    const uint16_t* ck;
-    const uint16_t* cv;
-    long c_rows;
     int layer, n_layers;
     const int32_t* route_off;
     const int32_t* route_res;
@@ -56,14 +60,15 @@ struct AttnF32Args {
     const float* k;
     const float* v;
     long k_rows;
-    const int32_t* cu_len;
-    const int32_t* pos_base;
-    RopeRev rope;
-    const int32_t* cu_q;
-    const int32_t* cu_ctx;
     const float* ck;
     const float* cv;
     long c_rows;
+    const int32_t* cu_len;
+    const int32_t* pos_base;
+    int p_len;  // encode: shared prefix rows in k / v; own rows in ck / cv
+    RopeRev rope;
+    const int32_t* cu_q;
+    const int32_t* cu_ctx;
     int layer, n_layers;
     const int32_t* route_off;
     const int32_t* route_res;

@@ -31,11 +31,11 @@ _SIGS = {
     "recache_rope_kv": ([_c_int, _c_int, _c_int, _c_int, _c_dbl, _c_p, _c_p, _c_p, _c_p, _c_p,
                          _c_int, _c_int, _c_p], _c_int),
     "recache_encode_resources": ([_c_int, _c_int, _c_p, _c_int, _c_int, _c_int, _c_int, _c_int,
-                                  _c_dbl, _c_p, _c_flt, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
-                                  _c_p], _c_int),
+                                  _c_dbl, _c_p, _c_int, _c_p, _c_p, _c_flt, _c_p, _c_p, _c_p,
+                                  _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_encode_attention": ([_c_int, _c_int, _c_p, _c_int, _c_int, _c_int, _c_int, _c_int,
-                                  _c_dbl, _c_p, _c_flt, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p],
-                                 _c_int),
+                                  _c_dbl, _c_p, _c_int, _c_p, _c_p, _c_flt, _c_p, _c_p, _c_p,
+                                  _c_p, _c_p, _c_p], _c_int),
     "recache_prune_gather": ([_c_int, _c_int, _c_p, _c_p, _c_p, _c_int, _c_int, _c_int, _c_int,
                               _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_build_routes": ([_c_int, _c_p, _c_p, _c_int, _c_int, _c_int, _c_int, _c_p, _c_p,
@@ -153,28 +153,43 @@ def rope_kv(k, v, pos, rope_base: float, k_cache, v_cache, row0: int = 0, stream
           k_cache.shape[1], row0, _stream(stream))
 
 
+def _prefix(prefix_k, prefix_v, like):
+    """(rows, k, v) of an optional shared prefix cache [Hkv][P][d]."""
+    if prefix_k is None and prefix_v is None:
+        return 0, None, None
+    if prefix_k is None or prefix_v is None or prefix_k.shape != prefix_v.shape:
+        raise ValueError("prefix_k and prefix_v must both be given, with one shape")
+    _same(like, prefix_k, prefix_v)
+    return prefix_k.shape[1], _dev(prefix_k, "prefix_k"), _dev(prefix_v, "prefix_v")
+
+
 def encode_resources(q, k, v, cu_len, max_len: int, rope_base: float, out, k_cache, v_cache,
-                     lse=None, pos_base=None, softmax_scale: float = 0.0, stream=None):
-    """One layer of block-diagonal resource encoding (see recache.h)."""
+                     lse=None, pos_base=None, softmax_scale: float = 0.0, stream=None,
+                     prefix_k=None, prefix_v=None):
+    """One layer of block-diagonal resource encoding (see recache.h), optionally
+    after a shared prefix whose rotated cache is prefix_k / prefix_v [Hkv][P][d]."""
     T, Hq, d = q.shape
     Hkv = k.shape[1]
     _same(q, k, v, out, k_cache, v_cache)
+    p_len, pk, pv = _prefix(prefix_k, prefix_v, q)
     _call("recache_encode_resources", _dtype_code(q), cu_len.numel() - 1,
           _dev(cu_len, "cu_len", _i32()), T, int(max_len), Hq, Hkv, d, rope_base,
-          _dev(pos_base, "pos_base", _i32()), softmax_scale, _dev(q, "q"), _dev(k, "k"),
-          _dev(v, "v"), _dev(out, "out"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
-          _dev(lse, "lse"), _stream(stream))
+          _dev(pos_base, "pos_base", _i32()), p_len, pk, pv, softmax_scale, _dev(q, "q"),
+          _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), _dev(k_cache, "k_cache"),
+          _dev(v_cache, "v_cache"), _dev(lse, "lse"), _stream(stream))
 
 
 def encode_attention(q, k_cache, v_cache, cu_len, max_len: int, rope_base: float, out, lse=None,
-                     pos_base=None, softmax_scale: float = 0.0, stream=None):
+                     pos_base=None, softmax_scale: float = 0.0, stream=None, prefix_k=None,
+                     prefix_v=None):
     """Attention half of the encode over already built caches [Hkv][T][d]."""
     T, Hq, d = q.shape
     Hkv = k_cache.shape[0]
     _same(q, k_cache, v_cache, out)
+    p_len, pk, pv = _prefix(prefix_k, prefix_v, q)
     _call("recache_encode_attention", _dtype_code(q), cu_len.numel() - 1,
           _dev(cu_len, "cu_len", _i32()), T, int(max_len), Hq, Hkv, d, rope_base,
-          _dev(pos_base, "pos_base", _i32()), softmax_scale, _dev(q, "q"),
+          _dev(pos_base, "pos_base", _i32()), p_len, pk, pv, softmax_scale, _dev(q, "q"),
           _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(out, "out"), _dev(lse, "lse"),
           _stream(stream))
 

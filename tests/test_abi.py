@@ -56,8 +56,8 @@ def test_check_kept():
 
 def enc(**kw):
     a = dict(dtype=1, n_res=2, cu_len=FAKE, total_T=10, max_len=6, Hq=32, Hkv=8, d=128,
-             base=1e6, pos_base=None, scale=0.0, q=FAKE, k=FAKE, v=FAKE, out=FAKE, kc=FAKE,
-             vc=FAKE, lse=None, stream=None)
+             base=1e6, pos_base=None, p_len=0, pk=None, pv=None, scale=0.0, q=FAKE, k=FAKE,
+             v=FAKE, out=FAKE, kc=FAKE, vc=FAKE, lse=None, stream=None)
     a.update(kw)
     return rc.lib().recache_encode_resources(*a.values())
 
@@ -75,6 +75,9 @@ def enc(**kw):
     (dict(cu_len=None), rc.EINVAL),
     (dict(base=0.5), rc.EINVAL),
     (dict(scale=float("nan")), rc.EINVAL),
+    (dict(p_len=-1), rc.EINVAL),
+    (dict(p_len=4), rc.EINVAL),  # prefix rows without prefix caches
+    (dict(p_len=4, pk=FAKE), rc.EINVAL),
 ])
 def test_encode_rejects(kw, code):
     assert enc(**kw) == code

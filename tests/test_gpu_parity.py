@@ -18,7 +18,7 @@ from paper_2608_19662_amd.workloads import (AttendWorkload, EncodeWorkload, conf
 pytestmark = pytest.mark.gpu
 
 
-def gpu_encode(w: EncodeWorkload, q, k, v, pos_base=None):
+def gpu_encode(w: EncodeWorkload, q, k, v, pos_base=None, prefix_k=None, prefix_v=None):
     T, Hq, d = q.shape
     Hkv = k.shape[1]
     out = torch.empty_like(q)
@@ -26,7 +26,8 @@ def gpu_encode(w: EncodeWorkload, q, k, v, pos_base=None):
     vc = torch.empty_like(kc)
     lse = torch.empty(Hq, T, dtype=torch.float32, device=DEV)
     rc.encode_resources(q, k, v, i32(w.cu_len), int(w.lengths.max()), w.rope_base, out, kc, vc,
-                        lse=lse, pos_base=None if pos_base is None else i32(pos_base))
+                        lse=lse, pos_base=None if pos_base is None else i32(pos_base),
+                        prefix_k=prefix_k, prefix_v=prefix_v)
     torch.cuda.synchronize()
     return out, kc, vc, lse
 
@@ -103,6 +104,79 @@ def test_encode_bf16_ragged(Hq, Hkv, d):
         o = int(w.cu_len[r])
         for h in range(Hq):
             assert torch.equal(out[o, h], vv[o, h // (Hq // Hkv)])
+
+
+def prefix_cache(seed, P, Hkv, d, dtype, base):
+    """A shared prefix's cache: keys rotated at 0..P-1 (by the library's own
+    RoPE entry point, as a serving stack would build it) and plain values."""
+    k = normal((P, Hkv, d), dtype, seed, 7, "cpu").to(DEV)
+    v = normal((P, Hkv, d), dtype, seed, 8, "cpu").to(DEV)
+    kc = torch.empty(Hkv, P, d, dtype=dtype, device=DEV)
+    vc = torch.empty_like(kc)
+    rc.rope_kv(k, v, i32(np.arange(P)), base, kc, vc)
+    torch.cuda.synchronize()
+    return kc, vc
+
+
+@pytest.mark.parametrize("Hq,Hkv,d,P,block", [(32, 8, 128, 100, False), (32, 8, 128, 1, False),
+                                               (8, 2, 64, 64, True), (28, 4, 128, 130, True)])
+def test_encode_prefix_bf16(Hq, Hkv, d, P, block):
+    """Resources encoded after a shared prefix (Sec. 3): every resource row sees
+    the whole prefix, then its own rows causally."""
+    print_case("encode prefix", Hq, Hkv, d, P, block)
+    w = EncodeWorkload(seed=14, lengths=np.array(ENC_LENGTHS, np.int32), n_q_heads=Hq,
+                       n_kv_heads=Hkv, head_dim=d, dtype="bf16", rope_base=1e6)
+    q, k, v = w.tensors("cpu")
+    pk, pv = prefix_cache(14, P, Hkv, d, torch.bfloat16, w.rope_base)
+    pb = (P + w.cu_len[:-1] if block else np.full(len(w.lengths), P)).astype(np.int32)
+    out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV), pos_base=pb,
+                                  prefix_k=pk, prefix_v=pv)
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base, pos_base=pb, prefix_k=pk.cpu(),
+                        prefix_v=pv.cpu())
+    check(out, ref["out"], "bf16", "out")
+    check(kc, ref["k_cache"], "bf16-ulp", "k_cache")
+    check(lse, ref["lse"], "bf16", "lse")
+
+
+def test_encode_prefix_composition_invariance_bitexact():
+    """With a shared prefix, a resource's outputs still do not depend on its
+    packing offset or neighbours (bit-exact)."""
+    print_case("encode prefix invariance")
+    lengths = np.array([300, 77, 513, 64, 129], np.int32)
+    w = EncodeWorkload(seed=15, lengths=lengths, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                       dtype="bf16", rope_base=1e6)
+    q, k, v = (t.to(DEV) for t in w.tensors("cpu"))
+    P = 77
+    pk, pv = prefix_cache(15, P, 8, 128, torch.bfloat16, w.rope_base)
+    pb = np.full(len(lengths), P, np.int32)
+    out, _, _, lse = gpu_encode(w, q, k, v, pos_base=pb, prefix_k=pk, prefix_v=pv)
+    perm = [3, 0, 4, 2, 1]
+    cu = w.cu_len
+    w2 = EncodeWorkload(seed=15, lengths=lengths[perm], n_q_heads=32, n_kv_heads=8, head_dim=128,
+                        dtype="bf16", rope_base=1e6)
+    cat = lambda t: torch.cat([t[cu[r]:cu[r + 1]] for r in perm]).contiguous()
+    out2, _, _, lse2 = gpu_encode(w2, cat(q), cat(k), cat(v), pos_base=pb, prefix_k=pk, prefix_v=pv)
+    cu2 = w2.cu_len
+    for j, r in enumerate(perm):
+        assert torch.equal(out[cu[r]:cu[r + 1]], out2[cu2[j]:cu2[j + 1]])
+        assert torch.equal(lse[:, cu[r]:cu[r + 1]], lse2[:, cu2[j]:cu2[j + 1]])
+
+
+def test_encode_prefix_fp32():
+    """The fp32 path with a shared prefix, at the stated fp32 bar."""
+    print_case("encode prefix fp32")
+    w = EncodeWorkload(seed=16, lengths=np.array([37, 64, 91, 120], np.int32), n_q_heads=8,
+                       n_kv_heads=2, head_dim=64, dtype="f32", rope_base=1e4)
+    q, k, v = w.tensors("cpu")
+    P = 20
+    pk, pv = prefix_cache(16, P, 2, 64, torch.float32, w.rope_base)
+    pb = np.full(4, P, np.int32)
+    out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV), pos_base=pb,
+                                  prefix_k=pk, prefix_v=pv)
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base, pos_base=pb, prefix_k=pk.cpu(),
+                        prefix_v=pv.cpu())
+    check(out, ref["out"], "f32", "out")
+    check(lse, ref["lse"], "f32", "lse")
 
 
 def test_encode_pos_base_shift():
