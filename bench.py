@@ -285,6 +285,94 @@ def prefix_encode_row(dev, reps, P=512):
             "pct_of_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
 
 
+def dense_prefill_row(dev, reps):
+    """Dense baseline of config 4's requests: each request's whole prompt
+    [its 8 resources, unpruned, then its 2048 context tokens] as one causal
+    sequence at global positions, 36 layers (one layer's tensors reused).
+    The attention of such a request is causal attention over the sequence, so
+    it runs on the encode kernel with one unit per request."""
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config, normal, prefix
+
+    w = config(4)["attend"]
+    L, Hq, Hkv, d = w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim
+    lens = np.array([int(w.lengths[w.req_res[w.req_res_off[b]:w.req_res_off[b + 1]]].sum())
+                     + int(w.ctx_lens[b]) for b in range(w.n_req)], np.int32)
+    N = int(lens.sum())
+    q = normal((N, Hq, d), torch.bfloat16, 4, 60, dev)
+    k = normal((N, Hkv, d), torch.bfloat16, 4, 61, dev)
+    v = normal((N, Hkv, d), torch.bfloat16, 4, 62, dev)
+    kc = torch.empty(Hkv, N, d, dtype=q.dtype, device=dev)
+    vc = torch.empty_like(kc)
+    cu = i32(prefix(lens), dev)
+    rc.rope_kv(k, v, i32(np.concatenate([np.arange(n) for n in lens]), dev), 1e6, kc, vc)
+    out = torch.empty_like(q)
+    n = lens.astype(np.int64)
+    flops = 4.0 * d * Hq * float(np.sum(n * (n + 1) // 2)) * L
+
+    def run():
+        for _ in range(L):
+            rc.encode_attention(q, kc, vc, cu, int(lens.max()), 1e6, out)
+
+    ms = timed(run, reps)
+    del q, k, v, kc, vc, out
+    torch.cuda.empty_cache()
+    return {"workload": "config 4 requests as dense causal prompts (%d tokens), 36 layers" % N,
+            "ms_per_pass": ms, "tflops": flops / (ms * 1e-3) / 1e12, "flops": flops,
+            "pct_of_peak": 100.0 * flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+
+def dense_decode_row(dev, reps):
+    """Dense baseline of config 5's decode: every resource row visible in every
+    (layer, group), nothing pruned, plus the 4096 context rows; 36 layers over
+    one layer's tensors (10 GB of K/V per layer)."""
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import config, normal
+
+    w = config(5)["attend"]
+    L, G, Hq, d = w.n_layers, w.n_kv_heads, w.n_q_heads, w.head_dim
+    R = int(w.cu_len[-1])
+    Tc = int(w.cu_ctx[-1])
+    q = normal((w.n_req, Hq, d), torch.bfloat16, 5, 70, dev)
+    ck = normal((G, Tc, d), torch.bfloat16, 5, 71, dev)
+    cv = normal((G, Tc, d), torch.bfloat16, 5, 72, dev)
+    rk = normal((G, R, d), torch.bfloat16, 5, 73, dev)
+    rv = normal((G, R, d), torch.bfloat16, 5, 74, dev)
+    E = w.n_req * L * G
+    cu_rows = i32(w.cu_len, dev)
+    route_off = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    route_res = torch.empty(int(w.req_res_off[-1]) * L * G, dtype=torch.int32, device=dev)
+    route_tokens = torch.empty(E, dtype=torch.int32, device=dev)
+    mask = torch.ones(w.n_res, L, G, dtype=torch.uint8, device=dev)
+    rc.build_routes(i32(w.req_res_off, dev), i32(w.req_res, dev), mask, cu_rows, route_off,
+                    route_res, route_tokens)
+    per_req = np.array([int(w.lengths[w.req_res[w.req_res_off[b]:w.req_res_off[b + 1]]].sum())
+                        for b in range(w.n_req)], np.int64)
+    keys = per_req + w.ctx_lens.astype(np.int64)
+    max_kv = int(keys.max())
+    nb = rc.attend_workspace_bytes(w.n_req, 1, int(w.ctx_lens.max()), max_kv, Hq, G, d)
+    ws = torch.empty(nb // 4, dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+    cu_q, cu_ctx = i32(w.cu_q, dev), i32(w.cu_ctx, dev)
+    max_route = int(np.diff(w.req_res_off).max())
+
+    def run():
+        for l in range(L):
+            rc.attend_cached(q, ck, cv, cu_q, cu_ctx, 1, int(w.ctx_lens.max()), rk, rv, cu_rows,
+                             route_off, route_res, route_tokens, l, L, out, workspace=ws,
+                             max_kv=max_kv, max_route_len=max_route)
+
+    ms = timed(run, reps)
+    nbytes = (float(keys.sum()) * G * 4 * d + 2.0 * w.n_req * Hq * d * 2) * L
+    del q, ck, cv, rk, rv, ws
+    torch.cuda.empty_cache()
+    return {"workload": "config 5 dense: all %d resource rows visible, unpruned" % R,
+            "ms_per_step": ms, "gbs": nbytes / (ms * 1e-3) / 1e9, "bytes": nbytes,
+            "pct_of_peak": 100.0 * nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+
+
 def cpu_baseline(w, tensors, min_seconds=10.0, max_passes=10):
     """The fp64 oracle on the headline workload: whole passes over all 16
     resources, repeated until about min_seconds of CPU time have been spent."""
@@ -359,6 +447,21 @@ def main():
             log("row a7_decode_config5 + a5_route_build")
             rows["a7_decode_config5"], rows["a5_route_build"] = decode_row(dev, args.reps)
             log("  ", json.dumps(rows["a7_decode_config5"]))
+        for name, fn in (("f2_dense_prefill_config4", lambda: dense_prefill_row(dev, args.reps)),
+                         ("f2_dense_decode_config5", lambda: dense_decode_row(dev, args.reps))):
+            if pick(name):
+                log("row", name)
+                rows[name] = fn()
+                log("  ", json.dumps(rows[name]))
+        # attention-time ratios Dense / ReCache on the same synthetic inputs
+        if "f2_dense_prefill_config4" in rows and "a6_prefill_config4" in rows:
+            rows["f2_dense_over_recache_prefill"] = round(
+                rows["f2_dense_prefill_config4"]["ms_per_pass"]
+                / rows["a6_prefill_config4"]["ms_per_pass"], 3)
+        if "f2_dense_decode_config5" in rows and "a7_decode_config5" in rows:
+            rows["f2_dense_over_recache_decode"] = round(
+                rows["f2_dense_decode_config5"]["ms_per_step"]
+                / rows["a7_decode_config5"]["ms_per_step"], 3)
         tensors = w.tensors(dev)
     cpu = None
     if not args.no_cpu_baseline:

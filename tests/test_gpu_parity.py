@@ -179,6 +179,23 @@ def test_encode_prefix_fp32():
     check(lse, ref["lse"], "f32", "lse")
 
 
+def test_dense_prompt_prefill_sampled_rows():
+    """The Dense baseline: whole prompts as single causal sequences at global
+    positions, through the encode kernel with one unit per prompt; sampled rows
+    against the oracle (a single-resource encode is textbook causal attention)."""
+    print_case("dense prompt prefill")
+    lengths = np.array([1500, 2100], np.int32)
+    w = EncodeWorkload(seed=17, lengths=lengths, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                       dtype="bf16", rope_base=1e6)
+    q, k, v = w.tensors("cpu")
+    out, kc, _, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
+    rows = np.concatenate([np.arange(0, 1500, 97), 1500 + np.arange(0, 2100, 131), [1499, 3599]])
+    check(out[rows], ref["out"][rows], "bf16", "out")
+    check(lse[:, rows], ref["lse"][:, rows], "bf16", "lse")
+    check(kc, ref["k_cache"], "bf16-ulp", "k_cache")
+
+
 def test_encode_pos_base_shift():
     """Explicit per-resource position bases (global 'Block' positions): the
     cache changes, the attention output does not (relative positions)."""
