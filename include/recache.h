@@ -228,6 +228,26 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           float* lse, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * [host] Structural budget selection (Sec. 3, "Structural Pruning").  From
+ * each layer's and each KV head group's leave-one-in contribution s_i (the
+ * drop in invocation loss when only that unit sees resource states), the
+ * contribution weights are w_i = max(s_i, 0) / sum_j max(s_j, 0); L* is the
+ * k_layers layers and G* the k_groups groups of largest weight (equal weights:
+ * lower index first), and the route set is Omega* = L* x G*.
+ *   route_mask[n_layers][n_groups]: 1 on Omega*, else 0 (the same for every
+ *       resource: copy it into recache_build_routes' [n_res][L][G] mask)
+ *   w_layer[n_layers], w_group[n_groups]: the contribution weights
+ *   rho = 1 - k_layers k_groups / (n_layers n_groups), the structural sparsity
+ *   cc_layer, cc_group: summed weight of the retained layers / groups (the
+ *       contribution coverage, as a fraction)
+ * Errors: RECACHE_EINVAL for counts < 1, a budget outside [0, n], a null
+ * pointer, a non-finite contribution, or no positive contribution in a kind.
+ */
+int recache_select_routes(int n_layers, int n_groups, const double* s_layer, const double* s_group,
+                          int k_layers, int k_groups, uint8_t* route_mask, double* w_layer,
+                          double* w_group, double* rho, double* cc_layer, double* cc_group);
+
+/*
  * [host] Validators for host copies of index arrays.  Return RECACHE_OK or
  * RECACHE_EINVAL (with recache_last_error() naming the first bad entry).
  *   recache_check_offsets: cu[0] = 0, cu non-decreasing (strictly increasing

@@ -9,6 +9,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "recache.h"
 #include "kernels.hpp"
 
@@ -488,3 +491,61 @@ int recache_check_kept(const int32_t* cu_len, const int32_t* cu_kept, const int3
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Structural budget selection (Sec. 3, "Structural Pruning"; rho and CC from
+// the structural budget analysis).  Host code.
+
+namespace {
+
+// w_i = max(s_i, 0) / sum_j max(s_j, 0); false if no s_i is positive or one is
+// not finite.
+bool contribution_weights(const double* s, int n, double* w) {
+    double total = 0.0;
+    for (int i = 0; i < n; ++i) {
+        if (!isfinite(s[i])) return false;
+        if (s[i] > 0.0) total += s[i];
+    }
+    if (!(total > 0.0)) return false;
+    for (int i = 0; i < n; ++i) w[i] = s[i] > 0.0 ? s[i] / total : 0.0;
+    return true;
+}
+
+// Units ranked by decreasing weight, equal weights by increasing index; keep[i]
+// is set for the first k.  Returns the kept weight.
+double keep_top(const double* w, int n, int k, std::vector<uint8_t>& keep) {
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return w[a] > w[b]; });
+    keep.assign(n, 0);
+    double cc = 0.0;
+    for (int r = 0; r < k; ++r) {
+        keep[order[r]] = 1;
+        cc += w[order[r]];
+    }
+    return cc;
+}
+
+}  // namespace
+
+int recache_select_routes(int n_layers, int n_groups, const double* s_layer, const double* s_group,
+                          int k_layers, int k_groups, uint8_t* route_mask, double* w_layer,
+                          double* w_group, double* rho, double* cc_layer, double* cc_group) {
+    REQUIRE(n_layers >= 1 && n_groups >= 1, RECACHE_EINVAL, "n_layers %d / n_groups %d must be >= 1",
+            n_layers, n_groups);
+    REQUIRE(k_layers >= 0 && k_layers <= n_layers && k_groups >= 0 && k_groups <= n_groups,
+            RECACHE_EINVAL, "budget %d x %d outside [0, %d] x [0, %d]", k_layers, k_groups, n_layers,
+            n_groups);
+    REQUIRE(s_layer && s_group && route_mask && w_layer && w_group && rho && cc_layer && cc_group,
+            RECACHE_EINVAL, "null pointer argument");
+    REQUIRE(contribution_weights(s_layer, n_layers, w_layer) &&
+                contribution_weights(s_group, n_groups, w_group),
+            RECACHE_EINVAL, "contributions must be finite, with a positive one among layers and groups");
+    std::vector<uint8_t> keep_l, keep_g;
+    *cc_layer = keep_top(w_layer, n_layers, k_layers, keep_l);
+    *cc_group = keep_top(w_group, n_groups, k_groups, keep_g);
+    for (int l = 0; l < n_layers; ++l)
+        for (int g = 0; g < n_groups; ++g) route_mask[(size_t)l * n_groups + g] = keep_l[l] & keep_g[g];
+    *rho = 1.0 - (double)k_layers * k_groups / ((double)n_layers * n_groups);
+    return ok();
+}

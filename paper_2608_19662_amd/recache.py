@@ -45,6 +45,8 @@ _SIGS = {
                                _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p, _c_p, _c_p,
                                _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                _c_p, _c_size, _c_p], _c_int),
+    "recache_select_routes": ([_c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p,
+                               _c_p, _c_p], _c_int),
     "recache_check_offsets": ([_c_p, _c_int, _c_int, _c_int], _c_int),
     "recache_check_kept": ([_c_p, _c_p, _c_p, _c_int], _c_int),
 }
@@ -254,3 +256,22 @@ def check_kept(cu_len, cu_kept, kept_idx) -> None:
     b = np.ascontiguousarray(np.asarray(cu_kept, dtype=np.int32))
     c = np.ascontiguousarray(np.asarray(kept_idx, dtype=np.int32))
     _call("recache_check_kept", a.ctypes.data, b.ctypes.data, c.ctypes.data, len(a) - 1)
+
+
+def select_routes(s_layer, s_group, k_layers: int, k_groups: int) -> dict:
+    """[host] Omega* = top-k_layers layers x top-k_groups groups by contribution
+    weight (see recache.h).  Returns route_mask[L][G] (uint8), the weights,
+    rho and the contribution coverages."""
+    import numpy as np
+
+    sl = np.ascontiguousarray(s_layer, dtype=np.float64)
+    sg = np.ascontiguousarray(s_group, dtype=np.float64)
+    L, G = len(sl), len(sg)
+    mask = np.zeros((L, G), np.uint8)
+    wl, wg = np.zeros(L), np.zeros(G)
+    out = (ctypes.c_double * 3)()
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    _call("recache_select_routes", L, G, p(sl), p(sg), int(k_layers), int(k_groups), p(mask),
+          p(wl), p(wg), ctypes.byref(out, 0), ctypes.byref(out, 8), ctypes.byref(out, 16))
+    return {"mask": mask, "w_layer": wl, "w_group": wg, "rho": out[0], "cc_layer": out[1],
+            "cc_group": out[2]}
