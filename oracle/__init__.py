@@ -202,24 +202,28 @@ def routes(req_res_off, req_res, mask, cu_kept):
 
 
 def attend(q, ctx_k, ctx_v, cu_q, cu_ctx, res_k, res_v, cu_rows, req_res_off, req_res, mask,
-           layer: int, scale: float | None = None, cu_kept=None, kept_idx=None, rows=None):
+           layer: int, scale: float | None = None, cu_kept=None, kept_idx=None, rows=None,
+           store_off=None):
     """Conversation queries over routed resources plus causal context, one layer.
 
     q[sum Tq][Hq][d] (rotated); ctx_k/ctx_v[Hkv][sum Tc][d]; res_k/res_v
     [Hkv][R][d] with resource r owning rows [cu_rows[r], cu_rows[r+1]);
     mask[n_res][L][G] uint8.  With kept_idx the visible rows of resource r are
     cu_rows[r] + kept_idx[cu_kept[r]:cu_kept[r+1]].  rows = (b_array, i_array)
-    picks which queries to evaluate (default: all).  Returns (out[n][Hq][d],
-    lse[n][Hq]) in float64.
+    picks which queries to evaluate (default: all).  With store_off (this
+    layer's row of :func:`store_offsets`), res_k/res_v are a route-compacted
+    store [rows][d] and resource r's rows for group g start at
+    store_off[r * G + g].  Returns (out[n][Hq][d], lse[n][Hq]) in float64.
     """
     q, ctx_k, ctx_v = host_view(q), host_view(ctx_k), host_view(ctx_v)
     res_k, res_v = host_view(res_k), host_view(res_v)
     cu_q, cu_ctx, cu_rows = _i32(cu_q), _i32(cu_ctx), _i32(cu_rows)
     req_res_off, req_res = _i32(req_res_off), _i32(req_res)
-    cu_kept, kept_idx = _i32(cu_kept), _i32(kept_idx)
+    cu_kept, kept_idx, store_off = _i32(cu_kept), _i32(kept_idx), _i32(store_off)
     mask = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
     n_res, L, G = mask.shape
     _, Hq, d = q.shape
+    res_stride = res_k.shape[1] if res_k.ndim == 3 else 0
     Hkv = ctx_k.shape[0]
     if G != Hkv:
         raise ValueError("mask groups %d != KV heads %d" % (G, Hkv))
@@ -238,9 +242,47 @@ def attend(q, ctx_k, ctx_v, cu_q, cu_ctx, res_k, res_v, cu_rows, req_res_off, re
         ctypes.c_int(_dtype_code(q)), ctypes.c_int(n_req), _p(cu_q), _p(cu_ctx),
         ctypes.c_int(Hq), ctypes.c_int(Hkv), ctypes.c_int(d), ctypes.c_double(scale),
         _p(q), _p(ctx_k), _p(ctx_v), ctypes.c_long(ctx_k.shape[1]),
-        ctypes.c_int(n_res), _p(cu_rows), ctypes.c_long(res_k.shape[1]), _p(res_k), _p(res_v),
+        ctypes.c_int(n_res), _p(cu_rows), ctypes.c_long(res_stride), _p(res_k), _p(res_v),
         _p(cu_kept), _p(kept_idx), _p(req_res_off), _p(req_res),
-        ctypes.c_int(L), ctypes.c_int(layer), _p(mask),
+        ctypes.c_int(L), ctypes.c_int(layer), _p(mask), _p(store_off),
         ctypes.c_int(n), _p(rb), _p(ri), _p(out), _p(lse))
     _check(rc, "attend")
     return out, lse
+
+
+def store_offsets(mask, cu_kept):
+    """Row tables of the route-compacted store: [L][n_res * G + 1] int32.
+
+    Entry [l][r * G + g] is where route (r, g) of layer l starts, the last
+    entry of a row the rows stored for that layer."""
+    mask = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+    cu_kept = _i32(cu_kept)
+    n_res, L, G = mask.shape
+    off = np.zeros((L, n_res * G + 1), np.int32)
+    rc = _load().oracle_store_offsets(ctypes.c_int(n_res), ctypes.c_int(L), ctypes.c_int(G),
+                                      _p(mask), _p(cu_kept), _p(off))
+    _check(rc, "store_offsets")
+    return off
+
+
+def store_routes(k_cache, v_cache, cu_len, cu_kept, kept_idx, mask, layer: int):
+    """One layer of the route-compacted store, gathered from head-major caches
+    [Hkv][T][d]: (k_store[rows][d], v_store[rows][d]), byte-exact copies."""
+    k_cache, v_cache = host_view(k_cache), host_view(v_cache)
+    cu_len, cu_kept, kept_idx = _i32(cu_len), _i32(cu_kept), _i32(kept_idx)
+    mask = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+    n_res, L, G = mask.shape
+    Hkv, _, d = k_cache.shape
+    if G != Hkv:
+        raise ValueError("mask groups %d != KV heads %d" % (G, Hkv))
+    kept = np.diff(cu_kept).astype(np.int64)
+    cap = max(1, int((mask[:, layer, :].sum(axis=1) * kept).sum()))
+    ks = np.empty((cap, d), k_cache.dtype)
+    vs = np.empty((cap, d), v_cache.dtype)
+    fn = _load().oracle_store_routes
+    fn.restype = ctypes.c_long
+    n = fn(ctypes.c_int(_dtype_code(k_cache)), ctypes.c_int(n_res), _p(cu_len), _p(cu_kept),
+           _p(kept_idx), ctypes.c_int(Hkv), ctypes.c_int(d), ctypes.c_int(L), ctypes.c_int(layer),
+           _p(mask), _p(k_cache), _p(v_cache), _p(ks), _p(vs), ctypes.c_long(cap))
+    _check(-1 if n < 0 else 0, "store_routes")
+    return ks[:n].copy(), vs[:n].copy()

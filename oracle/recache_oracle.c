@@ -27,6 +27,10 @@
  *   oracle_attend      -- conversation queries under the final ReCache mask
  *                         (Fig. 2 caption; Sec. 3 "Semantic Pruning", last
  *                         paragraph).
+ *   oracle_store_offsets, oracle_store_routes
+ *                      -- a resource store that holds state only for the
+ *                         visible routes (both pruning stages of Sec. 3; the
+ *                         memory column of the efficiency table counts it).
  *
  * Readings where the paper is silent (all listed in the design notes):
  *   RoPE pairs element i with element i + d/2 ("rotate half"); positions are
@@ -329,7 +333,10 @@ int oracle_routes(int n_req, const int32_t* req_res_off, const int32_t* req_res,
  * rows; resource r owns rows [cu_rows[r], cu_rows[r+1]).  If kept_idx is
  * given, the visible rows of resource r are cu_rows[r] + kept_idx[cu_kept[r]
  * + j] (semantic pruning applied by definition); otherwise every row of the
- * resource is visible (rows already compacted, or no pruning).
+ * resource is visible (rows already compacted, or no pruning).  If store_off
+ * is given (this layer's table from oracle_store_offsets), res_k / res_v are
+ * a route-compacted store [rows][d] instead, and the rows of resource r for
+ * group g are store_off[r * Hkv + g] + [0, cu_rows[r+1] - cu_rows[r]).
  *
  * For query i of request b (0-based within the request), head h and group
  * g = h / (Hq / Hkv), the keys are: every visible row of every resource of
@@ -359,7 +366,7 @@ int oracle_attend(int dtype, int n_req, const int32_t* cu_q, const int32_t* cu_c
                   const void* res_k, const void* res_v,
                   const int32_t* cu_kept, const int32_t* kept_idx,
                   const int32_t* req_res_off, const int32_t* req_res,
-                  int n_layers, int layer, const uint8_t* mask,
+                  int n_layers, int layer, const uint8_t* mask, const int32_t* store_off,
                   int n_rows, const int32_t* rows_b, const int32_t* rows_i,
                   double* out, double* lse) {
     if (n_req <= 0 || !cu_q || !cu_ctx || Hq <= 0 || Hkv <= 0 || Hq % Hkv || d <= 0 ||
@@ -368,6 +375,9 @@ int oracle_attend(int dtype, int n_req, const int32_t* cu_q, const int32_t* cu_c
         (n_rows && (!rows_b || !rows_i || !out)))
         return -1;
     if (kept_idx && oracle_check_kept(n_res, cu_rows, cu_kept, kept_idx)) return -1;
+    if (store_off && kept_idx) return -1;
+    /* A route-compacted store has no per-head planes: rows are absolute. */
+    if (store_off) res_stride = 0;
     const int ratio = Hq / Hkv;
     long max_keys = 0;
     for (int b = 0; b < n_req; ++b) {
@@ -402,7 +412,10 @@ int oracle_attend(int dtype, int n_req, const int32_t* cu_q, const int32_t* cu_c
             for (int j = req_res_off[b]; j < req_res_off[b + 1]; ++j) {
                 int r = req_res[j];
                 if (!mask[((size_t)r * n_layers + layer) * Hkv + g]) continue;
-                if (kept_idx) {
+                if (store_off) {
+                    for (int t = 0; t < cu_rows[r + 1] - cu_rows[r]; ++t)
+                        key_row[n++] = (int64_t)store_off[(size_t)r * Hkv + g] + t;
+                } else if (kept_idx) {
                     for (int t = cu_kept[r]; t < cu_kept[r + 1]; ++t)
                         key_row[n++] = (int64_t)cu_rows[r] + kept_idx[t];
                 } else {
@@ -429,4 +442,61 @@ int oracle_attend(int dtype, int n_req, const int32_t* cu_q, const int32_t* cu_c
         free(key_row);
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Route-compacted resource store.  After both pruning stages of Sec. 3 a
+ * resource's state is read only through the visible routes of Omega and only
+ * at its kept positions, so only those rows need storage: for layer l, every
+ * (resource r, KV group g) with mask[r][l][g] set holds the kept rows of r
+ * for head g, in kept order.  Routes are laid out resource-major, (r, g) in
+ * increasing r and then g, one table per layer:
+ *   store_off[l][r * G + g]  first row of route (r, g) (for an invisible route
+ *                            the row where it would start; it holds no rows),
+ *   store_off[l][n_res * G]  rows stored for layer l.
+ * The rows of a route are the kept count of r, cu_kept[r+1] - cu_kept[r].   */
+int oracle_store_offsets(int n_res, int L, int G, const uint8_t* mask, const int32_t* cu_kept,
+                         int32_t* store_off) {
+    if (n_res <= 0 || L <= 0 || G <= 0 || !mask || !cu_kept || !store_off) return -1;
+    const size_t stride = (size_t)n_res * G + 1;
+    for (int l = 0; l < L; ++l) {
+        int64_t run = 0;
+        for (int r = 0; r < n_res; ++r)
+            for (int g = 0; g < G; ++g) {
+                store_off[l * stride + (size_t)r * G + g] = (int32_t)run;
+                if (mask[((size_t)r * L + l) * G + g]) run += cu_kept[r + 1] - cu_kept[r];
+                if (run > INT32_MAX) return -1;
+            }
+        store_off[l * stride + (size_t)n_res * G] = (int32_t)run;
+    }
+    return 0;
+}
+
+/* Fill layer `layer` of the store straight from the constructed head-major
+ * caches [Hkv][T][d]: routes in (r, g) order, each appending the rows
+ * cu_len[r] + kept_idx[cu_kept[r] .. cu_kept[r+1]) of head g, copied byte for
+ * byte, into stores of cap_rows rows.  Returns the number of rows written
+ * (the store's layer size), or -1 (bad input, or more than cap_rows rows).  */
+long oracle_store_routes(int dtype, int n_res, const int32_t* cu_len, const int32_t* cu_kept,
+                         const int32_t* kept_idx, int Hkv, int d, int L, int layer,
+                         const uint8_t* mask, const void* k_cache, const void* v_cache,
+                         void* k_store, void* v_store, long cap_rows) {
+    if (oracle_check_kept(n_res, cu_len, cu_kept, kept_idx)) return -1;
+    if (Hkv <= 0 || d <= 0 || L <= 0 || layer < 0 || layer >= L || !mask || !k_cache ||
+        !v_cache || !k_store || !v_store)
+        return -1;
+    const size_t row = elem_size(dtype) * (size_t)d;
+    const int T = cu_len[n_res];
+    long n = 0;
+    for (int r = 0; r < n_res; ++r)
+        for (int g = 0; g < Hkv; ++g) {
+            if (!mask[((size_t)r * L + layer) * Hkv + g]) continue;
+            for (int j = cu_kept[r]; j < cu_kept[r + 1]; ++j, ++n) {
+                if (n >= cap_rows) return -1;
+                const size_t from = ((size_t)g * T + cu_len[r] + kept_idx[j]) * row;
+                memcpy((char*)k_store + (size_t)n * row, (const char*)k_cache + from, row);
+                memcpy((char*)v_store + (size_t)n * row, (const char*)v_cache + from, row);
+            }
+        }
+    return n;
 }

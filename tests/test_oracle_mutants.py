@@ -60,6 +60,15 @@ MUTANTS = {
     "encode_query_not_rounded": ("for (int e = 0; e < d; ++e) qr[e] = round_to(qr[e], rot_dtype);",
                                  ""),
     "rope_not_rounded": ("for (int e = 0; e < d; ++e) yr[e] = round_to(yr[e], rot_dtype);", ""),
+    "store_offsets_group_major": ("store_off[l * stride + (size_t)r * G + g] = (int32_t)run;",
+                                  "store_off[l * stride + (size_t)g * n_res + r] = (int32_t)run;"),
+    "store_offsets_count_routes": ("if (mask[((size_t)r * L + l) * G + g]) run += cu_kept[r + 1] - cu_kept[r];",
+                                   "if (mask[((size_t)r * L + l) * G + g]) run += 1;"),
+    "store_ignores_mask": ("if (!mask[((size_t)r * L + layer) * Hkv + g]) continue;", ""),
+    "store_wrong_head": ("const size_t from = ((size_t)g * T + cu_len[r] + kept_idx[j]) * row;",
+                         "const size_t from = ((size_t)0 * T + cu_len[r] + kept_idx[j]) * row;"),
+    "attend_store_group_major": ("key_row[n++] = (int64_t)store_off[(size_t)r * Hkv + g] + t;",
+                                 "key_row[n++] = (int64_t)store_off[(size_t)g * n_res + r] + t;"),
 }
 
 PINS = [
@@ -81,6 +90,10 @@ PINS = [
     pins.test_attend_decode_row_sees_every_context_row,
     pins.test_prune_matches_fancy_indexing_and_extremes,
     pins.test_routes_match_python_loops,
+    pins.test_store_offsets_closed_forms,
+    pins.test_store_routes_places_rows_where_offsets_say,
+    lambda: pins.test_attend_over_store_equals_attend_over_pruned_cache(44),
+    pins.test_store_size_factorises_for_a_shared_route_set,
 ]
 
 
