@@ -15,9 +15,14 @@
  *   recache_build_routes               per (request, layer, KV group) visible
  *                                      resource lists (Sec. 3, "Structural
  *                                      Pruning"; Fig. 2(b))
+ *   recache_route_store_offsets /      a resource store holding only visible
+ *   recache_store_routes               routes at kept positions (both pruning
+ *                                      stages; the memory it saves)
  *   recache_attend_cached              conversation queries over routed, kept
  *                                      resource rows plus causal context (final
  *                                      ReCache mask, Fig. 2)
+ *   recache_select_routes              [host] Omega* = L* x G* from contribution
+ *                                      scores, with sparsity and coverage
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -183,6 +188,43 @@ int recache_build_routes(int n_req, const int32_t* req_res_off, const int32_t* r
                          int32_t* route_res, int32_t* route_tokens, void* stream);
 
 /*
+ * Row tables of a route-compacted resource store (Sec. 3: after structural
+ * and semantic pruning a resource is read only through its visible routes
+ * and only at kept positions, so only those rows need memory; the memory
+ * column of the results tables counts this saving).  Layer l of the store
+ * holds, for every resource r and KV group g with route_mask[r][l][g] set,
+ * the kept rows of r for head g, resource-major: routes (r, g) in increasing
+ * r, then g.  Output, device int32, n_layers rows of n_res * n_kv_heads + 1:
+ *   store_off[l][r * n_kv_heads + g]: first store row of route (r, g) (an
+ *       invisible route holds no rows and gets the row where it would start)
+ *   store_off[l][n_res * n_kv_heads]: rows stored for layer l.
+ * A route holds cu_kept[r+1] - cu_kept[r] rows.  total_kept = cu_kept[n_res];
+ * n_kv_heads * total_kept must be below 2^31.  Exact and deterministic.
+ */
+int recache_route_store_offsets(int n_res, int n_layers, int n_kv_heads, int total_kept,
+                                const uint8_t* route_mask, const int32_t* cu_kept,
+                                int32_t* store_off, void* stream);
+
+/*
+ * Fill layer `layer` of a route-compacted store straight from that layer's
+ * constructed head-major caches (semantic-pruning gather and route
+ * compaction in one pass; Sec. 3, "Semantic Pruning" and "Structural
+ * Pruning"):
+ *   k_store[store_off[l][r * Hkv + g] + j] =
+ *       k_cache[g][cu_len[r] + kept_idx[cu_kept[r] + j]],  j < kept rows of r,
+ * for every visible route (r, g), and the same for v; rows are copied bit
+ * for bit.  store_off is the full table of recache_route_store_offsets;
+ * store_rows = store_off[layer][n_res * n_kv_heads] (read it back to size the
+ * store); k_store / v_store are [store_rows][head_dim].  kept lists follow
+ * recache_prune_gather's rules.
+ */
+int recache_store_routes(int dtype, int layer, int n_layers, int n_res, const int32_t* cu_len,
+                         const int32_t* cu_kept, const int32_t* kept_idx, int total_T,
+                         int total_kept, int n_kv_heads, int head_dim, const int32_t* store_off,
+                         int store_rows, const void* k_cache, const void* v_cache, void* k_store,
+                         void* v_store, void* stream);
+
+/*
  * Workspace bytes that recache_attend_cached needs for these sizes (0 when
  * max_q > 1: the prefill kernels use none).  max_kv is an upper bound on the
  * keys a (request, group) can see in one layer (route tokens + context), used
@@ -201,16 +243,21 @@ size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max
  * h and group g = h / (Hq / Hkv), the visible keys are, in this order:
  *   1. every kept row of every resource in route_res[route_off[e] ..
  *      route_off[e+1]) with e = (b * n_layers + layer) * n_kv_heads + g
- *      (rows res_k[g][cu_kept[r] .. cu_kept[r+1])) -- M_resource routes; an
- *      empty list is an M_context route;
+ *      (rows res_k[g][cu_kept[r] .. cu_kept[r+1]), or with a store table
+ *      rows res_k[res_off[r * n_kv_heads + g] + j], j < cu_kept[r+1] -
+ *      cu_kept[r]) -- M_resource routes; an empty list is an M_context route;
  *   2. context rows ctx_k[g][cu_ctx[b] + c] for c = 0 .. Tc_b - Tq_b + i
  *      (causal, bottom-right aligned; with Tq = 1 the new token sees all).
  *
  *   q[total_q][n_q_heads][head_dim]: rotated queries
  *   ctx_k/ctx_v[n_kv_heads][ctx_rows][head_dim]: rotated context K, context V
- *   res_k/res_v[n_kv_heads][res_rows][head_dim]: compacted kept rows of this
- *       layer (output of recache_prune_gather, or unpruned caches with
- *       cu_kept = cu_len)
+ *   res_k/res_v: this layer's resource rows, in one of two layouts:
+ *       res_off == NULL: [n_kv_heads][res_rows][head_dim] compacted kept rows
+ *           (output of recache_prune_gather, or unpruned caches with
+ *           cu_kept = cu_len);
+ *       res_off != NULL: a route-compacted store [res_rows][head_dim]
+ *           (recache_store_routes), res_off = this layer's row of
+ *           recache_route_store_offsets' table, res_rows its stored rows.
  *   route_off/route_res/route_tokens: output of recache_build_routes
  *   out[total_q][n_q_heads][head_dim]; lse[n_q_heads][total_q] or NULL
  *   max_route_len: upper bound on the resources of any route list (at most
@@ -223,9 +270,10 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           int max_route_len, int n_q_heads, int n_kv_heads, int head_dim,
                           float softmax_scale, const void* q, const void* ctx_k,
                           const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
-                          int res_rows, const int32_t* cu_kept, const int32_t* route_off,
-                          const int32_t* route_res, const int32_t* route_tokens, void* out,
-                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
+                          int res_rows, const int32_t* cu_kept, const int32_t* res_off,
+                          const int32_t* route_off, const int32_t* route_res,
+                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream);
 
 /*
  * [host] Structural budget selection (Sec. 3, "Structural Pruning").  From

@@ -195,6 +195,8 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
         a.k = static_cast<const uint16_t*>(prefix_k);
         a.v = static_cast<const uint16_t*>(prefix_v);
         a.k_rows = prefix_len;
+    a.k_gstride = prefix_len;
+        a.k_gstride = prefix_len;
         a.ck = static_cast<const uint16_t*>(k_cache);
         a.cv = static_cast<const uint16_t*>(v_cache);
         a.c_rows = total_T;
@@ -219,6 +221,7 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
     a.k = static_cast<const float*>(prefix_k);
     a.v = static_cast<const float*>(prefix_v);
     a.k_rows = prefix_len;
+    a.k_gstride = prefix_len;
     a.ck = static_cast<const float*>(k_cache);
     a.cv = static_cast<const float*>(v_cache);
     a.c_rows = total_T;
@@ -328,6 +331,49 @@ int recache_build_routes(int n_req, const int32_t* req_res_off, const int32_t* r
                       "recache_build_routes launch");
 }
 
+int recache_route_store_offsets(int n_res, int n_layers, int n_kv_heads, int total_kept,
+                                const uint8_t* route_mask, const int32_t* cu_kept,
+                                int32_t* store_off, void* stream) {
+    REQUIRE(n_res >= 1 && n_layers >= 1 && n_kv_heads >= 1, RECACHE_EINVAL,
+            "n_res %d, n_layers %d, n_kv_heads %d must be >= 1", n_res, n_layers, n_kv_heads);
+    REQUIRE(total_kept >= n_res, RECACHE_EINVAL, "total_kept %d < n_res %d", total_kept, n_res);
+    REQUIRE((long long)n_kv_heads * total_kept < 0x7fffffffLL &&
+                (long long)n_layers * ((long long)n_res * n_kv_heads + 1) <= 0x7fffffffLL,
+            RECACHE_EINVAL, "store tables would overflow int32");
+    REQUIRE(route_mask && cu_kept && store_off, RECACHE_EINVAL, "null pointer argument");
+    (void)hipGetLastError();
+    return hip_status(launch_store_offsets(n_res, n_layers, n_kv_heads, route_mask, cu_kept,
+                                           store_off, as_stream(stream)),
+                      "recache_route_store_offsets launch");
+}
+
+int recache_store_routes(int dtype, int layer, int n_layers, int n_res, const int32_t* cu_len,
+                         const int32_t* cu_kept, const int32_t* kept_idx, int total_T,
+                         int total_kept, int n_kv_heads, int head_dim, const int32_t* store_off,
+                         int store_rows, const void* k_cache, const void* v_cache, void* k_store,
+                         void* v_store, void* stream) {
+    int rc_ = check_dtype_dim(dtype, head_dim);
+    if (rc_) return rc_;
+    REQUIRE(n_res >= 1 && n_kv_heads >= 1, RECACHE_EINVAL, "n_res %d / n_kv_heads %d must be >= 1",
+            n_res, n_kv_heads);
+    REQUIRE(n_layers >= 1 && layer >= 0 && layer < n_layers, RECACHE_EINVAL,
+            "layer %d outside [0, %d)", layer, n_layers);
+    REQUIRE(total_T >= n_res, RECACHE_EINVAL, "total_T %d < n_res %d", total_T, n_res);
+    REQUIRE(total_kept >= n_res && total_kept <= total_T, RECACHE_EINVAL,
+            "total_kept %d outside [n_res, total_T] = [%d, %d]", total_kept, n_res, total_T);
+    REQUIRE(store_rows >= 0 && (long long)store_rows <= (long long)n_kv_heads * total_kept,
+            RECACHE_EINVAL, "store_rows %d outside [0, n_kv_heads * total_kept]", store_rows);
+    REQUIRE(cu_len && cu_kept && kept_idx && store_off && k_cache && v_cache &&
+                (store_rows == 0 || (k_store && v_store)),
+            RECACHE_EINVAL, "null pointer argument");
+    (void)hipGetLastError();
+    const int es = dtype == RECACHE_F32 ? 4 : 2;
+    return hip_status(launch_store_routes(es, layer, n_res, cu_len, cu_kept, kept_idx, total_T,
+                                          total_kept, n_kv_heads, head_dim, store_off, store_rows,
+                                          k_cache, v_cache, k_store, v_store, as_stream(stream)),
+                      "recache_store_routes launch");
+}
+
 size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max_kv,
                                       int n_q_heads, int n_kv_heads, int head_dim) {
     if (n_req <= 0 || max_q != 1 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 0;
@@ -340,9 +386,10 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           int max_route_len, int n_q_heads, int n_kv_heads, int head_dim,
                           float softmax_scale, const void* q, const void* ctx_k,
                           const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
-                          int res_rows, const int32_t* cu_kept, const int32_t* route_off,
-                          const int32_t* route_res, const int32_t* route_tokens, void* out,
-                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+                          int res_rows, const int32_t* cu_kept, const int32_t* res_off,
+                          const int32_t* route_off, const int32_t* route_res,
+                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream) {
     int rc_ = check_dtype_dim(dtype, head_dim);
     if (rc_) return rc_;
     if ((rc_ = check_heads(dtype, n_q_heads, n_kv_heads))) return rc_;
@@ -383,6 +430,8 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
         a.k = static_cast<const float*>(res_k);
         a.v = static_cast<const float*>(res_v);
         a.k_rows = res_rows;
+        a.k_gstride = res_off ? 0 : res_rows;
+        a.res_off = res_off;
         a.cu_q = cu_q;
         a.cu_ctx = cu_ctx;
         a.ck = static_cast<const float*>(ctx_k);
@@ -417,6 +466,8 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
         a.rk = static_cast<const uint16_t*>(res_k);
         a.rv = static_cast<const uint16_t*>(res_v);
         a.r_rows = res_rows;
+        a.r_gstride = res_off ? 0 : res_rows;
+        a.res_off = res_off;
         a.ck = static_cast<const uint16_t*>(ctx_k);
         a.cv = static_cast<const uint16_t*>(ctx_v);
         a.c_rows = ctx_rows;
@@ -445,6 +496,8 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
     a.k = static_cast<const uint16_t*>(res_k);
     a.v = static_cast<const uint16_t*>(res_v);
     a.k_rows = res_rows;
+    a.k_gstride = res_off ? 0 : res_rows;
+    a.res_off = res_off;
     a.cu_q = cu_q;
     a.cu_ctx = cu_ctx;
     a.ck = static_cast<const uint16_t*>(ctx_k);

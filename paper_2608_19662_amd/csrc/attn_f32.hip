@@ -83,20 +83,21 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const AttnF32Args a) {
 
     if constexpr (ENCODE) {
         // the shared prefix, fully visible, then the resource's own rows
-        const float* pk = a.k + (size_t)g * a.k_rows * d;
-        const float* pv = a.v + (size_t)g * a.k_rows * d;
+        const float* pk = a.k + (size_t)g * a.k_gstride * d;
+        const float* pv = a.v + (size_t)g * a.k_gstride * d;
         for (int u = 0; u < a.p_len; ++u) visit(pk + (size_t)u * d, pv + (size_t)u * d);
         const float* kb = a.ck + ((size_t)g * a.c_rows + q_row0) * d;
         const float* vb = a.cv + ((size_t)g * a.c_rows + q_row0) * d;
         for (int u = 0; u <= row; ++u) visit(kb + (size_t)u * d, vb + (size_t)u * d);
     } else {
         const size_t e = ((size_t)unit * a.n_layers + a.layer) * a.n_kv_heads + g;
-        const float* kb = a.k + (size_t)g * a.k_rows * d;
-        const float* vb = a.v + (size_t)g * a.k_rows * d;
+        const float* kb = a.k + (size_t)g * a.k_gstride * d;
+        const float* vb = a.v + (size_t)g * a.k_gstride * d;
         for (int s = a.route_off[e]; s < a.route_off[e + 1]; ++s) {
             const int r = a.route_res[s];
-            const int r_end = min(a.cu_kept[r + 1], (int)a.k_rows);
-            for (int u = a.cu_kept[r]; u < r_end; ++u) visit(kb + (size_t)u * d, vb + (size_t)u * d);
+            const int r_beg = a.res_off ? a.res_off[(size_t)r * a.n_kv_heads + g] : a.cu_kept[r];
+            const int r_end = min(r_beg + (a.cu_kept[r + 1] - a.cu_kept[r]), (int)a.k_rows);
+            for (int u = r_beg; u < r_end; ++u) visit(kb + (size_t)u * d, vb + (size_t)u * d);
         }
         const int c0 = a.cu_ctx[unit];
         const int tc = a.cu_ctx[unit + 1] - c0;

@@ -178,7 +178,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                 const int r = a.route_res[r0 + s];
                 const int k0 = a.cu_kept[r];
                 lens[i] = a.cu_kept[r + 1] - k0;
-                sm.seg_row[s] = k0;
+                sm.seg_row[s] = a.res_off ? a.res_off[(size_t)r * a.n_kv_heads + g] : k0;
             }
             part += lens[i];
         }
@@ -263,8 +263,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                 const long row0 = (long)u_dl + p0;
                 if (p0 + kBK <= u_hi && row0 >= 0 && row0 + kBK <= a.k_rows) {
                     t_fast = true;
-                    t_kb = a.k + ((size_t)g * a.k_rows + row0) * HD;
-                    t_vb = a.v + ((size_t)g * a.k_rows + row0) * HD;
+                    t_kb = a.k + ((size_t)g * a.k_gstride + row0) * HD;
+                    t_vb = a.v + ((size_t)g * a.k_gstride + row0) * HD;
                 }
             } else if (p0 >= s_vis && p0 + kBK <= stream) {
                 const long row0 = (long)ctx_row0 + (p0 - s_vis);
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                             seg_dl = sm.seg_row[sidx] - sm.seg_start[sidx];
                         }
                         const size_t row = min((size_t)(seg_dl + p), (size_t)a.k_rows - 1);
-                        kp[j] = (uint64_t)(a.k + ((size_t)g * a.k_rows + row) * HD + cp_chunk(j) * 8);
+                        kp[j] = (uint64_t)(a.k + ((size_t)g * a.k_gstride + row) * HD + cp_chunk(j) * 8);
                         in_ctx &= ~(1u << j);
                     } else {
                         const size_t row = min((size_t)ctx_row0 + (p - s_vis), (size_t)a.c_rows - 1);

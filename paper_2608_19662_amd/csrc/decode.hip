@@ -103,7 +103,7 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
             const int r = a.route_res[r0 + s];
             const int k0 = a.cu_kept[r];
             lens[i] = a.cu_kept[r + 1] - k0;
-            sm.seg_row[s] = k0;
+            sm.seg_row[s] = a.res_off ? a.res_off[(size_t)r * a.n_kv_heads + g] : k0;
         }
         part += lens[i];
     }
@@ -137,8 +137,8 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
     const int n_tiles = (s1 - s0 + kTk - 1) / kTk;
     __syncthreads();
 
-    const uint16_t* rk = a.rk + (size_t)g * a.r_rows * HD;
-    const uint16_t* rv = a.rv + (size_t)g * a.r_rows * HD;
+    const uint16_t* rk = a.rk + (size_t)g * a.r_gstride * HD;
+    const uint16_t* rv = a.rv + (size_t)g * a.r_gstride * HD;
     const uint16_t* ck = a.ck + (size_t)g * a.c_rows * HD;
     const uint16_t* cv = a.cv + (size_t)g * a.c_rows * HD;
     // Row of stream key p in its buffer (p < s_vis: kept resource rows, else

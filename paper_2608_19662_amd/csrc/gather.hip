@@ -4,7 +4,10 @@
 //     head-major buffer;
 //   - route lists (Sec. 3, "Structural Pruning"): for every (request, layer,
 //     KV group), the request's resources whose route is in Omega, in request
-//     order, as a CSR with a per-entry kept-token total.
+//     order, as a CSR with a per-entry kept-token total;
+//   - a route-compacted store (both pruning stages): per layer, only the
+//     visible (resource, group) routes hold rows, resource-major, each with
+//     the kept rows of its resource.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -102,7 +105,96 @@ __global__ __launch_bounds__(256) void route_fill_kernel(
     }
 }
 
+// One block per layer: exclusive scan over routes i = r * G + g of
+// mask[r][l][g] * kept_r, written to the layer's row of the table, plus the
+// layer's total.  Each thread scans a contiguous run of routes.
+__global__ __launch_bounds__(1024) void store_offsets_kernel(
+    int n_res, int L, int G, const uint8_t* __restrict__ mask,
+    const int32_t* __restrict__ cu_kept, int32_t* __restrict__ store_off) {
+    __shared__ int part[1024];
+    const int l = blockIdx.x, tid = threadIdx.x;
+    const long n = (long)n_res * G;
+    int32_t* off = store_off + (size_t)l * (n + 1);
+    const long per = (n + 1023) / 1024;
+    const long a = tid * per < n ? tid * per : n;
+    const long b = a + per < n ? a + per : n;
+    auto rows = [&](long i) {
+        const int r = (int)(i / G), g = (int)(i % G);
+        return mask[((size_t)r * L + l) * G + g] ? cu_kept[r + 1] - cu_kept[r] : 0;
+    };
+    int sum = 0;
+    for (long i = a; i < b; ++i) sum += rows(i);
+    part[tid] = sum;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+        const int add = tid >= o ? part[tid - o] : 0;
+        __syncthreads();
+        part[tid] += add;
+        __syncthreads();
+    }
+    int run = part[tid] - sum;
+    for (long i = a; i < b; ++i) {
+        off[i] = run;
+        run += rows(i);
+    }
+    if (tid == 1023) off[n] = part[1023];
+}
+
+// One thread per 16-byte chunk of a store row.  The route owning row u is the
+// last i with off[i] <= u: an invisible route has off[i] == off[i + 1], so the
+// last such i is the visible route whose rows contain u.
+__global__ __launch_bounds__(256) void store_routes_kernel(
+    int chunks_per_row, int G, const int32_t* __restrict__ off, int n_routes,
+    const int32_t* __restrict__ cu_len, const int32_t* __restrict__ cu_kept,
+    const int32_t* __restrict__ kept_idx, long total_T, long total_kept, long total_chunks,
+    const u32x4* __restrict__ kc, const u32x4* __restrict__ vc, u32x4* __restrict__ ko,
+    u32x4* __restrict__ vo) {
+    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total_chunks) return;
+    const int c = (int)(idx % chunks_per_row);
+    const int u = (int)(idx / chunks_per_row);
+    int lo = 0, hi = n_routes - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= u) lo = mid; else hi = mid - 1;
+    }
+    const int r = lo / G, g = lo % G;
+    long j = (long)cu_kept[r] + (u - off[lo]);
+    j = j < 0 ? 0 : (j >= total_kept ? total_kept - 1 : j);
+    long src = (long)cu_len[r] + kept_idx[j];
+    src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
+    const size_t s = ((size_t)g * total_T + src) * chunks_per_row + c;
+    ko[idx] = kc[s];
+    vo[idx] = vc[s];
+}
+
 }  // namespace
+
+hipError_t launch_store_offsets(int n_res, int n_layers, int n_kv_heads, const uint8_t* mask,
+                                const int32_t* cu_kept, int32_t* store_off, hipStream_t s) {
+    hipLaunchKernelGGL(store_offsets_kernel, dim3(n_layers), dim3(1024), 0, s, n_res, n_layers,
+                       n_kv_heads, mask, cu_kept, store_off);
+    return hipGetLastError();
+}
+
+hipError_t launch_store_routes(int elem_bytes, int layer, int n_res, const int32_t* cu_len,
+                               const int32_t* cu_kept, const int32_t* kept_idx, long total_T,
+                               long total_kept, int n_kv_heads, int head_dim,
+                               const int32_t* store_off, long store_rows, const void* k_cache,
+                               const void* v_cache, void* k_store, void* v_store, hipStream_t s) {
+    const int cpr = head_dim * elem_bytes / 16;
+    const long total = store_rows * cpr;
+    if (total == 0) return hipSuccess;
+    const long blocks = (total + 255) / 256;
+    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
+    const long n_routes = (long)n_res * n_kv_heads;
+    hipLaunchKernelGGL(store_routes_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr,
+                       n_kv_heads, store_off + (size_t)layer * (n_routes + 1), (int)n_routes,
+                       cu_len, cu_kept, kept_idx, total_T, total_kept, total,
+                       static_cast<const u32x4*>(k_cache), static_cast<const u32x4*>(v_cache),
+                       static_cast<u32x4*>(k_store), static_cast<u32x4*>(v_store));
+    return hipGetLastError();
+}
 
 hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
                                const int32_t* cu_kept, const int32_t* kept_idx, long total_T,

@@ -29,7 +29,8 @@ struct AttnArgs {
     // K / V caches; prefill: conversation context), all [n_kv_heads][rows][d].
     const uint16_t* k;
     const uint16_t* v;
-    long k_rows;        // rows per KV head in k / v
+    long k_rows;        // rows of one KV head's part of k / v (all rows with res_off)
+    long k_gstride;     // rows between KV heads in k / v (0 with res_off)
     const uint16_t* ck;
     const uint16_t* cv;
     long c_rows;        // rows per KV head in ck / cv
@@ -45,6 +46,7 @@ struct AttnArgs {
     const int32_t* route_off;
     const int32_t* route_res;
     const int32_t* cu_kept;
+    const int32_t* res_off;  // route-compacted store rows [n_res * Hkv], or NULL
 };
 hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream);
 
@@ -60,6 +62,7 @@ struct AttnF32Args {
     const float* k;
     const float* v;
     long k_rows;
+    long k_gstride;
     const float* ck;
     const float* cv;
     long c_rows;
@@ -73,6 +76,7 @@ struct AttnF32Args {
     const int32_t* route_off;
     const int32_t* route_res;
     const int32_t* cu_kept;
+    const int32_t* res_off;
 };
 hipError_t launch_attn_f32(const AttnF32Args& a, bool encode, hipStream_t stream);
 
@@ -100,6 +104,15 @@ hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
                                long total_kept, int n_kv_heads, int head_dim, const void* k_cache,
                                const void* v_cache, void* k_kept, void* v_kept, hipStream_t s);
 
+// Route-compacted store: row tables for every layer, then one layer's rows.
+hipError_t launch_store_offsets(int n_res, int n_layers, int n_kv_heads, const uint8_t* mask,
+                                const int32_t* cu_kept, int32_t* store_off, hipStream_t s);
+hipError_t launch_store_routes(int elem_bytes, int layer, int n_res, const int32_t* cu_len,
+                               const int32_t* cu_kept, const int32_t* kept_idx, long total_T,
+                               long total_kept, int n_kv_heads, int head_dim,
+                               const int32_t* store_off, long store_rows, const void* k_cache,
+                               const void* v_cache, void* k_store, void* v_store, hipStream_t s);
+
 // Route CSR build.
 hipError_t launch_build_routes(int n_req, const int32_t* req_res_off, const int32_t* req_res,
                                int n_res, int n_layers, int n_kv_heads, const uint8_t* mask,
@@ -116,7 +129,8 @@ struct DecodeArgs {
     long lse_rows;
     const uint16_t* rk;
     const uint16_t* rv;
-    long r_rows;
+    long r_rows;     // rows of one KV head's part of rk / rv (all rows with res_off)
+    long r_gstride;  // rows between KV heads in rk / rv (0 with res_off)
     const uint16_t* ck;
     const uint16_t* cv;
     long c_rows;
@@ -126,6 +140,7 @@ struct DecodeArgs {
     const int32_t* route_off;
     const int32_t* route_res;
     const int32_t* cu_kept;
+    const int32_t* res_off;  // route-compacted store rows [n_res * Hkv], or NULL
     float* ws_o;   // [n_req][Hq][n_splits][head_dim]
     float* ws_ml;  // [n_req][Hq][n_splits][2]  (max in log2 units, sum)
 };

@@ -41,10 +41,14 @@ _SIGS = {
     "recache_build_routes": ([_c_int, _c_p, _c_p, _c_int, _c_int, _c_int, _c_int, _c_p, _c_p,
                               _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_attend_workspace_bytes": ([_c_int] * 7, _c_size),
+    "recache_route_store_offsets": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p],
+                                    _c_int),
+    "recache_store_routes": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_p, _c_int, _c_int,
+                              _c_int, _c_int, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_attend_cached": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_int,
                                _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p, _c_p, _c_p,
                                _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
-                               _c_p, _c_size, _c_p], _c_int),
+                               _c_p, _c_p, _c_size, _c_p], _c_int),
     "recache_select_routes": ([_c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p,
                                _c_p, _c_p], _c_int),
     "recache_check_offsets": ([_c_p, _c_int, _c_int, _c_int], _c_int),
@@ -220,6 +224,42 @@ def build_routes(req_res_off, req_res, route_mask, cu_kept, route_off, route_res
           _dev(route_tokens, "route_tokens", _i32()), _stream(stream))
 
 
+def route_store_offsets(route_mask, cu_kept, store_off, total_kept: int | None = None,
+                        stream=None):
+    """Row tables of a route-compacted store: store_off is int32 [L][n_res * G + 1]."""
+    import torch
+
+    n_res, L, G = route_mask.shape
+    if total_kept is None:
+        total_kept = _total(cu_kept)
+    _call("recache_route_store_offsets", n_res, L, G, int(total_kept),
+          _dev(route_mask, "route_mask", (torch.uint8,)), _dev(cu_kept, "cu_kept", _i32()),
+          _dev(store_off, "store_off", _i32()), _stream(stream))
+
+
+def _total(cu):
+    """Last entry of a device offsets array (one small device-to-host copy)."""
+    return int(cu[-1].item())
+
+
+def store_routes(k_cache, v_cache, cu_len, cu_kept, kept_idx, store_off, layer: int, k_store,
+                 v_store, total_kept: int | None = None, stream=None):
+    """One layer of a route-compacted store from head-major caches [Hkv][T][d].
+
+    k_store / v_store are [rows][d] with rows = store_off[layer][-1]."""
+    Hkv, T, d = k_cache.shape
+    _same(k_cache, v_cache, k_store, v_store)
+    L = store_off.shape[0]
+    if total_kept is None:
+        total_kept = _total(cu_kept)
+    _call("recache_store_routes", _dtype_code(k_cache), layer, L, cu_len.numel() - 1,
+          _dev(cu_len, "cu_len", _i32()), _dev(cu_kept, "cu_kept", _i32()),
+          _dev(kept_idx, "kept_idx", _i32()), T, int(total_kept), Hkv, d,
+          _dev(store_off, "store_off", _i32()), k_store.shape[0], _dev(k_cache, "k_cache"),
+          _dev(v_cache, "v_cache"), _dev(k_store, "k_store"), _dev(v_store, "v_store"),
+          _stream(stream))
+
+
 def attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads, n_kv_heads, head_dim) -> int:
     return int(lib().recache_attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads,
                                                     n_kv_heads, head_dim))
@@ -228,18 +268,22 @@ def attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads, n_kv_heads,
 def attend_cached(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k, res_v, cu_kept,
                   route_off, route_res, route_tokens, layer: int, n_layers: int, out, lse=None,
                   workspace=None, max_kv: int = 0, max_route_len: int = 1024,
-                  softmax_scale: float = 0.0, stream=None):
-    """Conversation queries over routed kept resource rows + causal context (one layer)."""
+                  softmax_scale: float = 0.0, res_off=None, stream=None):
+    """Conversation queries over routed kept resource rows + causal context (one layer).
+
+    res_k / res_v are [Hkv][rows][d] kept rows, or with res_off (this layer's
+    row of a store table) a route-compacted store [rows][d]."""
     total_q, Hq, d = q.shape
     Hkv = ctx_k.shape[0]
+    res_rows = res_k.shape[0] if res_off is not None else res_k.shape[1]
     _same(q, ctx_k, ctx_v, res_k, res_v, out)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("recache_attend_cached", _dtype_code(q), layer, n_layers, cu_q.numel() - 1,
           _dev(cu_q, "cu_q", _i32()), _dev(cu_ctx, "cu_ctx", _i32()), total_q, int(max_q),
           int(max_ctx), int(max_kv), int(max_route_len), Hq, Hkv, d, softmax_scale, _dev(q, "q"),
           _dev(ctx_k, "ctx_k"), _dev(ctx_v, "ctx_v"), ctx_k.shape[1], _dev(res_k, "res_k"),
-          _dev(res_v, "res_v"), res_k.shape[1], _dev(cu_kept, "cu_kept", _i32()),
-          _dev(route_off, "route_off", _i32()), _dev(route_res, "route_res", _i32()),
+          _dev(res_v, "res_v"), res_rows, _dev(cu_kept, "cu_kept", _i32()),
+          _dev(res_off, "res_off", _i32()), _dev(route_off, "route_off", _i32()), _dev(route_res, "route_res", _i32()),
           _dev(route_tokens, "route_tokens", _i32()), _dev(out, "out"), _dev(lse, "lse"),
           _dev(workspace, "workspace"), ws_bytes, _stream(stream))
 

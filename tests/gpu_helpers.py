@@ -96,12 +96,22 @@ class Routes:
                                       w.n_kv_heads, w.head_dim)
         return torch.empty(max(n, 4) // 4, dtype=torch.float32, device=DEV) if n else None
 
-    def attend(self, q, ck, cv, rk, rv, layer, lse=True, workspace=None, max_kv=0, stream=None):
+    def attend(self, q, ck, cv, rk, rv, layer, lse=True, workspace=None, max_kv=0, stream=None,
+               res_off=None):
         w = self.w
         out = torch.empty_like(q)
         l = torch.empty(w.n_q_heads, q.shape[0], dtype=torch.float32, device=DEV) if lse else None
         rc.attend_cached(q, ck, cv, self.cu_q, self.cu_ctx, self.max_q, self.max_ctx, rk, rv,
                          self.cu_rows, self.route_off, self.route_res, self.route_tokens, layer,
                          w.n_layers, out, lse=l, workspace=workspace, max_kv=max_kv,
-                         max_route_len=max(self.max_route_len, 1), stream=stream)
+                         max_route_len=max(self.max_route_len, 1), stream=stream,
+                         res_off=res_off)
         return out, l
+
+    def store_offsets(self):
+        """GPU-built row tables of the route-compacted store, [L][n_res * G + 1]."""
+        w = self.w
+        off = torch.empty(w.n_layers, len(w.lengths) * w.n_kv_heads + 1, dtype=torch.int32,
+                          device=DEV)
+        rc.route_store_offsets(self.mask, self.cu_rows, off, total_kept=int(w.cu_rows[-1]))
+        return off

@@ -94,7 +94,7 @@ def att(**kw):
     a = dict(dtype=1, layer=0, n_layers=36, n_req=2, cu_q=FAKE, cu_ctx=FAKE, total_q=2, max_q=1,
              max_ctx=16, max_kv=0, max_route_len=32, Hq=32, Hkv=8, d=128, scale=0.0, q=FAKE,
              ck=FAKE, cv=FAKE, ctx_rows=32, rk=FAKE, rv=FAKE, res_rows=8, cu_kept=FAKE,
-             route_off=FAKE, route_res=FAKE, route_tokens=FAKE, out=FAKE, lse=None,
+             res_off=None, route_off=FAKE, route_res=FAKE, route_tokens=FAKE, out=FAKE, lse=None,
              ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return rc.lib().recache_attend_cached(*a.values())
@@ -138,6 +138,40 @@ def test_prune_and_routes_reject():
                                   None) == rc.EINVAL
     assert L.recache_rope_kv(1, 8, 8, 128, 1e4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 4,
                              None) == rc.EINVAL  # rows [4, 12) overflow 10
+
+
+def store(**kw):
+    a = dict(dtype=1, layer=0, n_layers=36, n_res=4, cu_len=FAKE, cu_kept=FAKE, kept_idx=FAKE,
+             T=100, kept=30, Hkv=8, d=128, off=FAKE, rows=60, kc=FAKE, vc=FAKE, ks=FAKE,
+             vs=FAKE, stream=None)
+    a.update(kw)
+    return rc.lib().recache_store_routes(*a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(layer=36), rc.EINVAL),
+    (dict(kept=101), rc.EINVAL),          # more kept rows than rows
+    (dict(kept=3), rc.EINVAL),            # fewer than one per resource
+    (dict(rows=241), rc.EINVAL),          # more than every route of every kept row
+    (dict(rows=-1), rc.EINVAL),
+    (dict(off=None), rc.EINVAL),
+    (dict(ks=None), rc.EINVAL),
+    (dict(d=96), rc.EUNSUPPORTED),
+    (dict(dtype=7), rc.EUNSUPPORTED),
+])
+def test_store_routes_rejects(kw, code):
+    assert store(**kw) == code
+    assert rc.last_error()
+
+
+def test_store_offsets_rejects():
+    L = rc.lib()
+    assert L.recache_route_store_offsets(0, 36, 8, 10, FAKE, FAKE, FAKE, None) == rc.EINVAL
+    assert L.recache_route_store_offsets(4, 36, 8, 3, FAKE, FAKE, FAKE, None) == rc.EINVAL
+    assert L.recache_route_store_offsets(4, 36, 8, 2 ** 28, FAKE, FAKE, FAKE, None) == rc.EINVAL
+    assert L.recache_route_store_offsets(4, 36, 8, 10, None, FAKE, FAKE, None) == rc.EINVAL
+    # an empty store is valid and launches nothing
+    assert store(rows=0, ks=None, vs=None) == rc.OK
 
 
 def test_python_binding_refuses_host_tensors():

@@ -492,3 +492,105 @@ def test_decode_full_size_layers():
         check(lse, rlse.T, "bf16", "lse")
         del q, ck, cv, rk, rv
         torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------- route-compacted store
+
+def kept_lists(w):
+    """(cu_kept, kept_idx) of a workload; an unpruned one keeps every row."""
+    if w.kept_idx is not None:
+        return w.cu_kept, w.kept_idx
+    return w.cu_len, np.concatenate([np.arange(n) for n in w.lengths]).astype(np.int32)
+
+
+@pytest.mark.parametrize("k", [3, 4, 5])
+def test_store_offsets_bitexact_full_size(k):
+    print_case("store offsets", k)
+    w = config(k)["attend"]
+    off = Routes(w).store_offsets()
+    torch.cuda.synchronize()
+    assert np.array_equal(off.cpu().numpy(), oracle.store_offsets(w.mask, w.cu_rows))
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 128)])
+def test_store_routes_bitexact(dtype, d):
+    """Config 4's structure (64 resources, 36 layers, 25 % of routes, 30 %
+    kept): three layers of the store gathered from unpruned caches."""
+    print_case("store routes", dtype, d)
+    w = config(4)["attend"]
+    T = int(w.cu_len[-1])
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    kc = normal((8, T, d), dt, 60, 1, DEV)
+    vc = normal((8, T, d), dt, 60, 2, DEV)
+    off = Routes(w).store_offsets()
+    off_h = off.cpu().numpy()
+    for layer in (0, 17, 35):
+        rows = int(off_h[layer, -1])
+        ks = torch.empty(rows, d, dtype=dt, device=DEV)
+        vs = torch.empty_like(ks)
+        rc.store_routes(kc, vc, i32(w.cu_len), i32(w.cu_kept), i32(w.kept_idx), off, layer, ks,
+                        vs)
+        torch.cuda.synchronize()
+        rk, rv = oracle.store_routes(kc.cpu(), vc.cpu(), w.cu_len, w.cu_kept, w.kept_idx, w.mask,
+                                     layer)
+        assert np.array_equal(oracle.host_view(ks.cpu()), rk)
+        assert np.array_equal(oracle.host_view(vs.cpu()), rv)
+
+
+def run_store_case(w, layer):
+    """Attend over a route-compacted store built on the GPU from unpruned
+    caches: bit-identical to attend over the per-head kept rows (same keys in
+    the same order), and within tolerance of the oracle reading the store."""
+    rt = Routes(w)
+    q, ck, cv, kc, vc = w.layer_tensors(layer, DEV, compacted=False)
+    cu_kept, kept_idx = kept_lists(w)
+    off = rt.store_offsets()
+    off_h = off.cpu().numpy()
+    rows = int(off_h[layer, -1])
+    ks = torch.empty(max(rows, 1), w.head_dim, dtype=kc.dtype, device=DEV)
+    vs = torch.empty_like(ks)
+    rc.store_routes(kc, vc, i32(w.cu_len), i32(cu_kept), i32(kept_idx), off, layer, ks[:rows],
+                    vs[:rows])
+    K = int(cu_kept[-1])
+    kk = torch.empty(w.n_kv_heads, K, w.head_dim, dtype=kc.dtype, device=DEV)
+    vk = torch.empty_like(kk)
+    rc.prune_gather(kc, vc, i32(w.cu_len), i32(cu_kept), i32(kept_idx), kk, vk)
+    max_kv = rt.max_kv(layer)
+    ws = rt.workspace(max_kv)
+    out_s, lse_s = rt.attend(q, ck, cv, ks, vs, layer, workspace=ws, max_kv=max_kv,
+                             res_off=off[layer])
+    out_h, lse_h = rt.attend(q, ck, cv, kk, vk, layer, workspace=ws, max_kv=max_kv)
+    torch.cuda.synchronize()
+    assert torch.equal(out_s, out_h) and torch.equal(lse_s, lse_h)
+    rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, ks.cpu()[:rows],
+                               vs.cpu()[:rows], cu_kept, w.req_res_off, w.req_res, w.mask, layer,
+                               store_off=off_h[layer])
+    check(out_s, rout, w.dtype, "store attend out")
+    check(lse_s, rlse.T, w.dtype, "store attend lse")
+
+
+@pytest.mark.parametrize("case", [PREFILL_CASES[0], PREFILL_CASES[1], PREFILL_CASES[5],
+                                  DECODE_CASES[0], DECODE_CASES[2], DECODE_CASES[6]])
+def test_attend_over_route_store(case):
+    seed, n_req, pool, Hq, Hkv, d, ql, cl = case
+    print_case("store attend", case)
+    w = small_attend(seed, n_req, pool, Hq, Hkv, d, "bf16", ql, cl, max_len=600)
+    for layer in range(w.n_layers):
+        run_store_case(w, layer)
+
+
+def test_attend_over_route_store_fp32_and_unpruned():
+    print_case("store attend fp32 / unpruned")
+    run_store_case(small_attend(53, 3, 5, 8, 2, 128, "f32", [20, 1, 7], [20, 30, 40]), 1)
+    run_store_case(small_attend(54, 2, 5, 8, 2, 64, "f32", [1, 1], [1, 90]), 0)
+    run_store_case(small_attend(55, 3, 6, 32, 8, 128, "bf16", [40, 64, 1], [100, 64, 9],
+                                prune=False), 2)
+
+
+def test_decode_full_size_over_route_store():
+    """Config 5 at full size, one layer, resource state in a route-compacted
+    store (only the visible 25 % of routes, 30 % of rows): every output."""
+    print_case("decode full store")
+    w = config(5)["attend"]
+    run_store_case(w, 11)
+    torch.cuda.empty_cache()
