@@ -214,6 +214,86 @@ def decode_row(dev, reps):
                  "entries": int(w.n_req * L * G)}
 
 
+def route_store_row(dev, reps):
+    """Config 5 with resource state in a route-compacted store: row tables,
+    the fused kept-row + route gather of every layer, decode over the store,
+    and the allocated resource-KV bytes against the unpruned all-route cache
+    (and, for the paper's Omega*_{20,3} of Qwen3-4B, the same accounting)."""
+    import torch
+    from paper_2608_19662_amd import recache as rc
+    from paper_2608_19662_amd.workloads import (OMEGA_20_3_QWEN3_4B_GROUPS,
+                                                OMEGA_20_3_QWEN3_4B_LAYERS, config, normal,
+                                                omega_star_mask)
+
+    w = config(5)["attend"]
+    L, G, d = w.n_layers, w.n_kv_heads, w.head_dim
+    n_res = len(w.lengths)
+    T, K = int(w.cu_len[-1]), int(w.cu_kept[-1])
+    st = _routes(w, dev)
+    mask_d = st["args"][2]
+    off = torch.empty(L, n_res * G + 1, dtype=torch.int32, device=dev)
+    off_ms = timed(lambda: rc.route_store_offsets(mask_d, st["cu_rows"], off, total_kept=K), reps)
+    rows = off[:, -1].cpu().numpy().astype(np.int64)
+    # one layer's constructed caches serve as the gather source of every layer
+    kc = normal((G, T, d), torch.bfloat16, 5, 950, dev)
+    vc = normal((G, T, d), torch.bfloat16, 5, 951, dev)
+    ks = [torch.empty(int(n), d, dtype=torch.bfloat16, device=dev) for n in rows]
+    vs = [torch.empty_like(t) for t in ks]
+    idx = (i32(w.cu_len, dev), st["cu_rows"], i32(w.kept_idx, dev))
+
+    def build():
+        for l in range(L):
+            rc.store_routes(kc, vc, *idx, off, l, ks[l], vs[l], total_kept=K)
+
+    build_ms = timed(build, reps)
+    build_bytes = 2.0 * 2 * float(rows.sum()) * d * 2  # read + write of K and V rows
+    del kc, vc
+    torch.cuda.empty_cache()
+
+    s_vis = visible_tokens(w)
+    keys = s_vis + w.ctx_lens.astype(np.int64)[:, None, None]
+    io_bytes = float(keys.sum()) * 2 * d * 2 + 2.0 * L * w.n_req * w.n_q_heads * d * 2
+    max_kv = int(keys.max())
+    layers = [w.layer_tensors(l, dev)[:3] for l in range(L)]
+    torch.cuda.empty_cache()
+    outs = [torch.empty_like(t[0]) for t in layers]
+    nb = rc.attend_workspace_bytes(w.n_req, 1, int(w.ctx_lens.max()), max_kv, w.n_q_heads, G, d)
+    ws = torch.empty(nb // 4, dtype=torch.float32, device=dev)
+
+    def run():
+        for l in range(L):
+            q, ck, cv = layers[l]
+            rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], 1, int(w.ctx_lens.max()), ks[l],
+                             vs[l], st["cu_rows"], st["route_off"], st["route_res"],
+                             st["route_tokens"], l, L, outs[l], workspace=ws, max_kv=max_kv,
+                             max_route_len=st["max_route_len"], res_off=off[l])
+
+    ms = timed(run, reps)
+    gbs = io_bytes / (ms * 1e-3) / 1e9
+    row_bytes = 2 * d * 2  # K and V, bf16
+    unpruned = float(L * G * T * row_bytes)
+    all_routes = float(L * G * K * row_bytes)
+    stored = float(rows.sum() * row_bytes)
+    paper_mask = omega_star_mask(n_res, L, G, OMEGA_20_3_QWEN3_4B_LAYERS,
+                                 OMEGA_20_3_QWEN3_4B_GROUPS)
+    kept = np.diff(w.cu_kept).astype(np.int64)
+    paper_rows = float(np.einsum("r,rlg->", kept, paper_mask.astype(np.int64)))
+    res = {"workload": "config 5, resource state in a route-compacted store", "layers": L,
+           "ms_per_step": ms, "gbs": gbs, "pct_of_peak": 100.0 * gbs / PEAK_HBM_GBS,
+           "bytes": io_bytes, "store_offsets_ms": off_ms, "store_build_ms_36_layers": build_ms,
+           "store_build_gbs": build_bytes / (build_ms * 1e-3) / 1e9,
+           "mem": {"unpruned_all_routes_gb": unpruned / 1e9,
+                   "kept_all_routes_gb": all_routes / 1e9,
+                   "route_store_gb": stored / 1e9,
+                   "reduction_vs_unpruned_pct": 100.0 * (1 - stored / unpruned),
+                   "omega_20_3_qwen3_4b_store_gb": paper_rows * row_bytes / 1e9,
+                   "omega_20_3_qwen3_4b_reduction_pct":
+                       100.0 * (1 - paper_rows * row_bytes / unpruned)}}
+    del layers, outs, ks, vs
+    torch.cuda.empty_cache()
+    return res
+
+
 def prune_row(dev, reps):
     import torch
     from paper_2608_19662_amd import recache as rc
@@ -447,6 +527,10 @@ def main():
             log("row a7_decode_config5 + a5_route_build")
             rows["a7_decode_config5"], rows["a5_route_build"] = decode_row(dev, args.reps)
             log("  ", json.dumps(rows["a7_decode_config5"]))
+        if pick("f3_route_store_config5"):
+            log("row f3_route_store_config5")
+            rows["f3_route_store_config5"] = route_store_row(dev, args.reps)
+            log("  ", json.dumps(rows["f3_route_store_config5"]))
         for name, fn in (("f2_dense_prefill_config4", lambda: dense_prefill_row(dev, args.reps)),
                          ("f2_dense_decode_config5", lambda: dense_decode_row(dev, args.reps))):
             if pick(name):

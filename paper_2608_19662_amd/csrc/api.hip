@@ -404,10 +404,11 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
             (long)n_req * max_q);
     REQUIRE(max_route_len >= 0 && max_route_len <= 1024, RECACHE_EUNSUPPORTED,
             "max_route_len %d outside [0, 1024]", max_route_len);
-    REQUIRE(ctx_rows >= 1 && res_rows >= 1, RECACHE_EINVAL, "ctx_rows %d / res_rows %d must be >= 1",
-            ctx_rows, res_rows);
-    REQUIRE(cu_q && cu_ctx && q && ctx_k && ctx_v && res_k && res_v && cu_kept && route_off &&
-                route_res && route_tokens && out,
+    // a route-compacted store may hold no rows for a layer outside every route
+    REQUIRE(ctx_rows >= 1 && res_rows >= (res_off ? 0 : 1), RECACHE_EINVAL,
+            "ctx_rows %d / res_rows %d too small", ctx_rows, res_rows);
+    REQUIRE(cu_q && cu_ctx && q && ctx_k && ctx_v && ((res_k && res_v) || res_rows == 0) &&
+                cu_kept && route_off && route_res && route_tokens && out,
             RECACHE_EINVAL, "null pointer argument");
     REQUIRE(!(isnan(softmax_scale) || isinf(softmax_scale)), RECACHE_EINVAL, "softmax_scale not finite");
     const float scale = resolve_scale(softmax_scale, head_dim);

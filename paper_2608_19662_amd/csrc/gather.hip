@@ -140,32 +140,51 @@ __global__ __launch_bounds__(1024) void store_offsets_kernel(
     if (tid == 1023) off[n] = part[1023];
 }
 
-// One thread per 16-byte chunk of a store row.  The route owning row u is the
-// last i with off[i] <= u: an invisible route has off[i] == off[i + 1], so the
-// last such i is the visible route whose rows contain u.
+// One block per route i = r * G + g of the layer: a visible route copies
+// the kept rows of r for head g to store rows off[i] .. off[i + 1]; an
+// invisible route (no rows) exits at once.  Each thread moves U 16-byte
+// chunks per step, all loads issued before the stores.
 __global__ __launch_bounds__(256) void store_routes_kernel(
-    int chunks_per_row, int G, const int32_t* __restrict__ off, int n_routes,
+    int chunks_per_row, int G, const int32_t* __restrict__ off,
     const int32_t* __restrict__ cu_len, const int32_t* __restrict__ cu_kept,
-    const int32_t* __restrict__ kept_idx, long total_T, long total_kept, long total_chunks,
+    const int32_t* __restrict__ kept_idx, long total_T, long total_kept, long store_rows,
     const u32x4* __restrict__ kc, const u32x4* __restrict__ vc, u32x4* __restrict__ ko,
     u32x4* __restrict__ vo) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= total_chunks) return;
-    const int c = (int)(idx % chunks_per_row);
-    const int u = (int)(idx / chunks_per_row);
-    int lo = 0, hi = n_routes - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (off[mid] <= u) lo = mid; else hi = mid - 1;
+    constexpr int U = 4;
+    const int i = blockIdx.x;
+    const int o0 = off[i];
+    const int n_rows = off[i + 1] - o0;
+    if (n_rows <= 0 || o0 < 0) return;
+    const int r = i / G, g = i % G;
+    const long k0 = cu_kept[r];
+    const long row0 = (long)g * total_T;
+    const long beg = cu_len[r];
+    // rows past the end of the store (an inconsistent table) are not written
+    const int n = (int)min((long)n_rows, store_rows - o0) * chunks_per_row;
+    for (int c0 = threadIdx.x; c0 < n; c0 += 256 * U) {
+        u32x4 kx[U], vx[U];
+        size_t dst[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = min(c0 + u * 256, n - 1);
+            const int sh = __builtin_ctz(chunks_per_row);  // a power of two
+            const int j = c >> sh, e = c & (chunks_per_row - 1);
+            const long kj = min(k0 + j, total_kept - 1);
+            long src = beg + kept_idx[kj];
+            src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
+            const size_t s = (size_t)(row0 + src) * chunks_per_row + e;
+            kx[u] = kc[s];
+            vx[u] = vc[s];
+            dst[u] = (size_t)(o0 + j) * chunks_per_row + e;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (c0 + u * 256 < n) {
+                ko[dst[u]] = kx[u];
+                vo[dst[u]] = vx[u];
+            }
+        }
     }
-    const int r = lo / G, g = lo % G;
-    long j = (long)cu_kept[r] + (u - off[lo]);
-    j = j < 0 ? 0 : (j >= total_kept ? total_kept - 1 : j);
-    long src = (long)cu_len[r] + kept_idx[j];
-    src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
-    const size_t s = ((size_t)g * total_T + src) * chunks_per_row + c;
-    ko[idx] = kc[s];
-    vo[idx] = vc[s];
 }
 
 }  // namespace
@@ -182,17 +201,15 @@ hipError_t launch_store_routes(int elem_bytes, int layer, int n_res, const int32
                                long total_kept, int n_kv_heads, int head_dim,
                                const int32_t* store_off, long store_rows, const void* k_cache,
                                const void* v_cache, void* k_store, void* v_store, hipStream_t s) {
+    if (store_rows == 0) return hipSuccess;
     const int cpr = head_dim * elem_bytes / 16;
-    const long total = store_rows * cpr;
-    if (total == 0) return hipSuccess;
-    const long blocks = (total + 255) / 256;
-    if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     const long n_routes = (long)n_res * n_kv_heads;
-    hipLaunchKernelGGL(store_routes_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr,
-                       n_kv_heads, store_off + (size_t)layer * (n_routes + 1), (int)n_routes,
-                       cu_len, cu_kept, kept_idx, total_T, total_kept, total,
-                       static_cast<const u32x4*>(k_cache), static_cast<const u32x4*>(v_cache),
-                       static_cast<u32x4*>(k_store), static_cast<u32x4*>(v_store));
+    if (n_routes > 0x7fffffffL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(store_routes_kernel, dim3((unsigned)n_routes), dim3(256), 0, s, cpr,
+                       n_kv_heads, store_off + (size_t)layer * (n_routes + 1), cu_len, cu_kept,
+                       kept_idx, total_T, total_kept, store_rows, static_cast<const u32x4*>(k_cache),
+                       static_cast<const u32x4*>(v_cache), static_cast<u32x4*>(k_store),
+                       static_cast<u32x4*>(v_store));
     return hipGetLastError();
 }
 

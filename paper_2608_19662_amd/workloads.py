@@ -59,6 +59,22 @@ def draw_route_mask_bernoulli(rng, n_res: int, L: int, G: int, p: float) -> np.n
     return (rng.random((n_res, L, G)) < p).astype(np.uint8)
 
 
+# Omega*_{20,3} of Qwen3-4B, the paper's primary backbone (36 layers, 8 KV
+# groups): the 20 layers and 3 groups of largest contribution weight in its
+# appendix table of per-layer and per-group weights, 0-based.  Qwen3-4B has
+# the 36-layer, 32/8-head, d-128 attention shape of the decode workload.
+OMEGA_20_3_QWEN3_4B_LAYERS = (13, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 26, 27, 29, 30, 31, 32,
+                              33, 34, 35)
+OMEGA_20_3_QWEN3_4B_GROUPS = (2, 3, 5)
+
+
+def omega_star_mask(n_res: int, L: int, G: int, layers, groups) -> np.ndarray:
+    """The same route set L* x G* for every resource, as a [n_res][L][G] mask."""
+    m = np.zeros((n_res, L, G), np.uint8)
+    m[:, np.asarray(layers)[:, None], np.asarray(groups)[None, :]] = 1
+    return m
+
+
 def draw_kept(rng, lengths, frac: float):
     """Kept-token lists: the final token of every resource, plus a uniform
     sample without replacement of the others, k_i = max(1, floor(frac*D_i + 0.5))

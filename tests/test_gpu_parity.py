@@ -13,7 +13,7 @@ import oracle
 from gpu_helpers import DEV, Routes, check, f64, i32
 from paper_2608_19662_amd import recache as rc
 from paper_2608_19662_amd.workloads import (AttendWorkload, EncodeWorkload, config, draw_kept,
-                                            draw_lengths, normal, prefix)
+                                            draw_lengths, normal, omega_star_mask, prefix)
 
 pytestmark = pytest.mark.gpu
 
@@ -547,10 +547,9 @@ def run_store_case(w, layer):
     off = rt.store_offsets()
     off_h = off.cpu().numpy()
     rows = int(off_h[layer, -1])
-    ks = torch.empty(max(rows, 1), w.head_dim, dtype=kc.dtype, device=DEV)
+    ks = torch.empty(rows, w.head_dim, dtype=kc.dtype, device=DEV)
     vs = torch.empty_like(ks)
-    rc.store_routes(kc, vc, i32(w.cu_len), i32(cu_kept), i32(kept_idx), off, layer, ks[:rows],
-                    vs[:rows])
+    rc.store_routes(kc, vc, i32(w.cu_len), i32(cu_kept), i32(kept_idx), off, layer, ks, vs)
     K = int(cu_kept[-1])
     kk = torch.empty(w.n_kv_heads, K, w.head_dim, dtype=kc.dtype, device=DEV)
     vk = torch.empty_like(kk)
@@ -562,8 +561,8 @@ def run_store_case(w, layer):
     out_h, lse_h = rt.attend(q, ck, cv, kk, vk, layer, workspace=ws, max_kv=max_kv)
     torch.cuda.synchronize()
     assert torch.equal(out_s, out_h) and torch.equal(lse_s, lse_h)
-    rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, ks.cpu()[:rows],
-                               vs.cpu()[:rows], cu_kept, w.req_res_off, w.req_res, w.mask, layer,
+    rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, ks.cpu(),
+                               vs.cpu(), cu_kept, w.req_res_off, w.req_res, w.mask, layer,
                                store_off=off_h[layer])
     check(out_s, rout, w.dtype, "store attend out")
     check(lse_s, rlse.T, w.dtype, "store attend lse")
@@ -585,6 +584,17 @@ def test_attend_over_route_store_fp32_and_unpruned():
     run_store_case(small_attend(54, 2, 5, 8, 2, 64, "f32", [1, 1], [1, 90]), 0)
     run_store_case(small_attend(55, 3, 6, 32, 8, 128, "bf16", [40, 64, 1], [100, 64, 9],
                                 prune=False), 2)
+
+
+def test_attend_over_route_store_with_empty_layer():
+    """One route set L* x G* for every resource (as the paper's Omega*):
+    layers outside L* store no rows at all and read context only."""
+    print_case("store attend, shared route set with an empty layer")
+    for ql, cl in (([30, 1, 65], [60, 40, 65]), ([1, 1, 1], [7, 300, 64])):
+        w = small_attend(56, 3, 6, 32, 8, 128, "bf16", ql, cl, max_len=400)
+        w.mask = omega_star_mask(len(w.lengths), w.n_layers, 8, (0, 2), (1, 4, 6))
+        for layer in range(w.n_layers):
+            run_store_case(w, layer)
 
 
 def test_decode_full_size_over_route_store():

@@ -13,6 +13,8 @@ import pytest
 
 from oracle import budget
 from paper_2608_19662_amd import recache as rc
+from paper_2608_19662_amd.workloads import (OMEGA_20_3_QWEN3_4B_GROUPS, OMEGA_20_3_QWEN3_4B_LAYERS,
+                                            omega_star_mask)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "structural_budget_weights.json")
 MODELS = ("Qwen3-4B", "Qwen3-1.7B")
@@ -64,12 +66,17 @@ def test_oracle_reproduces_printed_budget(model):
 
 
 def test_qwen3_4b_route_set():
-    """Omega*_{20,3} of the primary backbone, as 0-based (layer, group) sets."""
+    """Omega*_{20,3} of the primary backbone, as 0-based (layer, group) sets,
+    and the constant the workloads carry for it."""
     m, wl, wg = load("Qwen3-4B")
     sel = budget.select_routes(wl, wg, 20, 3)
     assert sel["layers"] == [13, 15, 16, 17, 18, 19, 20, 21, 22, 23, 24, 26, 27, 29, 30, 31, 32,
                              33, 34, 35]
     assert sel["groups"] == [2, 3, 5]
+    assert list(OMEGA_20_3_QWEN3_4B_LAYERS) == sel["layers"]
+    assert list(OMEGA_20_3_QWEN3_4B_GROUPS) == sel["groups"]
+    mask = omega_star_mask(4, 36, 8, OMEGA_20_3_QWEN3_4B_LAYERS, OMEGA_20_3_QWEN3_4B_GROUPS)
+    assert np.array_equal(mask[2], sel["mask"])
 
 
 def test_oracle_weights_closed_forms():
