@@ -121,3 +121,47 @@ def test_pins_catch_mutant(name, source, tmp_path, monkeypatch):
         except (AssertionError, ValueError):
             caught.append(getattr(pin, "__name__", "lambda"))
     assert caught, "mutant %s survived every pin" % name
+
+
+# ------------------------------------------------------------------ route-budget oracle
+
+import test_route_budget as budget_pins  # noqa: E402
+
+BUDGET_SRC = os.path.join(os.path.dirname(oracle.__file__), "budget.py")
+
+BUDGET_MUTANTS = {
+    "negative_contributions_kept": ("pos = np.where(s > 0, s, 0.0)", "pos = s"),
+    "ties_to_higher_index": ("key=lambda i: (-w[i], i)", "key=lambda i: (-w[i], -i)"),
+    "smallest_weights_kept": ("key=lambda i: (-w[i], i)", "key=lambda i: (w[i], i)"),
+    "sparsity_additive": ("1.0 - (k_layers * k_groups) / (L * G)",
+                          "1.0 - (k_layers + k_groups) / (L + G)"),
+    "coverage_of_everything": ("float(sum(wl[i] for i in ls))", "float(sum(wl))"),
+    "budget_off_by_one": ("return sorted(order[:k])", "return sorted(order[:k + 1])"),
+    "unnormalised": ("return pos / total", "return pos"),
+}
+
+BUDGET_PINS = [
+    lambda: budget_pins.test_oracle_reproduces_printed_budget("Qwen3-4B"),
+    lambda: budget_pins.test_oracle_reproduces_printed_budget("Qwen3-1.7B"),
+    budget_pins.test_qwen3_4b_route_set,
+    budget_pins.test_oracle_weights_closed_forms,
+]
+
+
+@pytest.mark.parametrize("name", sorted(BUDGET_MUTANTS))
+def test_budget_pins_catch_mutant(name, monkeypatch):
+    import types
+
+    old, new = BUDGET_MUTANTS[name]
+    src = open(BUDGET_SRC).read()
+    assert src.count(old) == 1, "mutation target not found exactly once: %r" % old
+    mod = types.ModuleType("budget_mutant")
+    exec(compile(src.replace(old, new), "budget_mutant.py", "exec"), mod.__dict__)
+    monkeypatch.setattr(budget_pins, "budget", mod)
+    caught = []
+    for pin in BUDGET_PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError, IndexError):
+            caught.append(getattr(pin, "__name__", "lambda"))
+    assert caught, "mutant %s survived every pin" % name
