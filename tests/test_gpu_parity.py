@@ -273,6 +273,25 @@ def test_config2_full_size_sampled_resources():
         assert torch.equal(vc[:, a:b], v[a:b].permute(1, 0, 2))
 
 
+def test_encode_long_resource_among_single_tokens():
+    """One 4100-token resource (65 query tiles, a ragged last tile) packed
+    between single-token resources, GQA 8/2, d 128: the long resource against
+    the oracle, the single tokens return their own value rows."""
+    print_case("encode long resource")
+    w = EncodeWorkload(seed=57, lengths=np.array([1, 4100, 1, 1, 33], np.int32), n_q_heads=8,
+                       n_kv_heads=2, head_dim=128, dtype="bf16", rope_base=1e6)
+    q, k, v = w.tensors(DEV)
+    out, kc, vc, lse = gpu_encode(w, q, k, v)
+    cu = w.cu_len
+    a, b = int(cu[1]), int(cu[2])
+    ref = oracle.encode(q[a:b].cpu(), k[a:b].cpu(), v[a:b].cpu(), [0, b - a], w.rope_base)
+    check(out[a:b], ref["out"], "bf16", "out")
+    check(lse[:, a:b], ref["lse"], "bf16", "lse")
+    for r in (0, 2, 3):
+        t = int(cu[r])
+        assert torch.equal(out[t].view(2, 4, 128), v[t][:, None, :].expand(2, 4, 128))
+
+
 # ---------------------------------------------------------------- prune and routes
 
 @pytest.mark.parametrize("k", [4, 5])
@@ -438,6 +457,36 @@ def test_decode_deterministic():
     a = run_attend_case(w, 0)
     b = run_attend_case(w, 0)
     assert torch.equal(a, b)
+
+
+def many_segments(seed, q_lens, ctx_lens, n_res=1024, Hq=32, Hkv=8):
+    """Every request lists all n_res tiny resources (1 to 4 tokens, a random
+    non-empty subset kept), every route visible: the route lists reach the
+    1024-resource limit and most 64-key tiles span many segments."""
+    rng = np.random.default_rng(seed)
+    lengths = rng.integers(1, 5, size=n_res).astype(np.int32)
+    kept = []
+    for D in lengths:
+        k = int(rng.integers(1, D + 1))
+        kept.append(np.sort(rng.choice(int(D), size=k, replace=False)).astype(np.int32))
+    reqs = [rng.permutation(n_res) for _ in q_lens]
+    return AttendWorkload(seed=seed, n_layers=2, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=128,
+                          dtype="bf16", lengths=lengths, req_res_off=prefix([len(r) for r in reqs]),
+                          req_res=np.concatenate(reqs).astype(np.int32),
+                          q_lens=np.asarray(q_lens, np.int32), ctx_lens=np.asarray(ctx_lens, np.int32),
+                          mask=np.ones((n_res, 2, Hkv), np.uint8),
+                          cu_kept=prefix([len(x) for x in kept]), kept_idx=np.concatenate(kept))
+
+
+@pytest.mark.parametrize("ql,cl", [([70, 1], [100, 5]), ([1, 1, 1], [1, 300, 64])])
+def test_attend_route_lists_at_the_resource_limit(ql, cl):
+    """1024 visible resources per route list, prefill and decode, both the
+    per-head kept cache and the route-compacted store."""
+    print_case("1024 segments", ql, cl)
+    w = many_segments(58, ql, cl)
+    for layer in range(2):
+        run_attend_case(w, layer)
+    run_store_case(w, 1)
 
 
 # ---------------------------------------------------------------- full-size attend configs
