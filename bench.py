@@ -90,10 +90,28 @@ def headline(args, dev):
     rope_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     flops = encode_flops(w)
     ms = wall * 1e3 / args.steps
+    # The working set (about 330 MB) exceeds the 256 MB last-level cache, so
+    # back-to-back steps still find part of it there.  For reference, time
+    # steps that each follow a 512 MB write (outside the timed interval),
+    # which leaves none of the inputs in that cache.
+    flush = torch.empty(512 << 18, dtype=torch.float32, device=dev)
+    cold = []
+    for _ in range(10):
+        flush.fill_(1.0)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        step(e)
+        torch.cuda.synchronize()
+        cold.append(e[0].elapsed_time(e[2]))
+    del flush
+    cold_ms = float(np.median(cold))
     return w, {
         "flops": flops, "ms_per_step": ms, "tflops": flops / (ms * 1e-3) / 1e12,
         "attn_ms": attn_ms, "rope_ms": rope_ms, "tokens": T,
         "pairs_per_head": w.pairs_per_head(),
+        "cold_cache": {"ms_per_step": round(cold_ms, 5),
+                       "tflops": round(flops / (cold_ms * 1e-3) / 1e12, 3),
+                       "note": "median of 10 steps, each after a 512 MB write that evicts the "
+                               "inputs from the last-level cache; rope_kv + attention events"},
     }, (q, k, v)
 
 
@@ -586,6 +604,7 @@ def main():
             "avg_kernel_ms": round(h["attn_ms"], 5),
         },
         "cpu_baseline": cpu,
+        "cold_cache": h["cold_cache"],
         "rows": rows,
     }
     print(json.dumps(line), flush=True)
