@@ -592,12 +592,16 @@ int recache_select_routes(int n_layers, int n_groups, const double* s_layer, con
             n_groups);
     REQUIRE(s_layer && s_group && route_mask && w_layer && w_group && rho && cc_layer && cc_group,
             RECACHE_EINVAL, "null pointer argument");
-    REQUIRE(contribution_weights(s_layer, n_layers, w_layer) &&
-                contribution_weights(s_group, n_groups, w_group),
+    // weights into local buffers first: no output is written on an error
+    std::vector<double> wl(n_layers), wg(n_groups);
+    REQUIRE(contribution_weights(s_layer, n_layers, wl.data()) &&
+                contribution_weights(s_group, n_groups, wg.data()),
             RECACHE_EINVAL, "contributions must be finite, with a positive one among layers and groups");
     std::vector<uint8_t> keep_l, keep_g;
-    *cc_layer = keep_top(w_layer, n_layers, k_layers, keep_l);
-    *cc_group = keep_top(w_group, n_groups, k_groups, keep_g);
+    *cc_layer = keep_top(wl.data(), n_layers, k_layers, keep_l);
+    *cc_group = keep_top(wg.data(), n_groups, k_groups, keep_g);
+    std::copy(wl.begin(), wl.end(), w_layer);
+    std::copy(wg.begin(), wg.end(), w_group);
     for (int l = 0; l < n_layers; ++l)
         for (int g = 0; g < n_groups; ++g) route_mask[(size_t)l * n_groups + g] = keep_l[l] & keep_g[g];
     *rho = 1.0 - (double)k_layers * k_groups / ((double)n_layers * n_groups);

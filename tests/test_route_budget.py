@@ -111,7 +111,25 @@ def test_library_matches_oracle(model):
 
 def test_library_rejects_bad_budgets():
     for args in (([1.0], [1.0], 2, 1), ([1.0], [1.0], 1, -1), ([-1.0], [1.0], 1, 1),
-                 ([float("nan")], [1.0], 1, 1)):
+                 ([float("nan")], [1.0], 1, 1), ([1.0], [0.0, -2.0], 1, 1)):
         with pytest.raises(rc.RecacheError) as e:
             rc.select_routes(*args)
         assert e.value.code == rc.EINVAL
+
+
+def test_library_writes_nothing_on_error():
+    """Valid layer contributions, invalid group ones: every output keeps its
+    previous contents."""
+    import ctypes
+
+    L, G = 3, 2
+    sl = np.array([1.0, 2.0, 3.0])
+    sg = np.array([-1.0, 0.0])
+    mask = np.full(L * G, 7, np.uint8)
+    wl, wg = np.full(L, -5.0), np.full(G, -5.0)
+    out = np.full(3, -5.0)
+    p = lambda a: a.ctypes.data
+    code = rc.lib().recache_select_routes(L, G, p(sl), p(sg), 1, 1, p(mask), p(wl), p(wg), p(out),
+                                          ctypes.c_void_p(p(out) + 8), ctypes.c_void_p(p(out) + 16))
+    assert code == rc.EINVAL
+    assert (mask == 7).all() and (wl == -5.0).all() and (wg == -5.0).all() and (out == -5.0).all()
