@@ -37,11 +37,15 @@
  *   (except RECACHE_EHIP, which reports a launch failure).
  *   recache_last_error() returns the text for the last non-OK status of the
  *   calling thread.
- * - Device index arrays (offsets, kept lists, route lists) are trusted by the
- *   kernels: pass them through recache_check_offsets / recache_check_kept on a
- *   host copy when they come from an untrusted source.  Kernels clamp every
- *   address they form to the extents given as scalars, so bad device indices
- *   give wrong numbers, never accesses outside the buffers.
+ * - Device index arrays (offsets, kept lists, route lists, store tables) are
+ *   trusted by the kernels: pass them through recache_check_offsets /
+ *   recache_check_kept on a host copy when they come from an untrusted source.
+ *   Kernels clamp every row address of Q, K, V, O and the caches to the extents
+ *   given as scalars, so bad row indices give wrong numbers, not accesses
+ *   outside those buffers.  The index arrays must agree with each other (route
+ *   lists and store tables as recache_build_routes and
+ *   recache_route_store_offsets write them), since one is read at positions
+ *   another names.
  * - Element types: RECACHE_F32 (float) or RECACHE_BF16 (bfloat16); all
  *   floating tensors of one call share the dtype.  bf16 math accumulates in
  *   fp32; outputs are rounded to nearest even.  head_dim is 64 or 128.

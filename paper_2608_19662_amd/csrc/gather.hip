@@ -160,15 +160,16 @@ __global__ __launch_bounds__(256) void store_routes_kernel(
     const long row0 = (long)g * total_T;
     const long beg = cu_len[r];
     // rows past the end of the store (an inconsistent table) are not written
-    const int n = (int)min((long)n_rows, store_rows - o0) * chunks_per_row;
-    for (int c0 = threadIdx.x; c0 < n; c0 += 256 * U) {
+    const long n = min((long)n_rows, store_rows - o0) * chunks_per_row;
+    for (long c0 = threadIdx.x; c0 < n; c0 += 256 * U) {
         u32x4 kx[U], vx[U];
         size_t dst[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = min(c0 + u * 256, n - 1);
+            const long c = min(c0 + u * 256, n - 1);
             const int sh = __builtin_ctz(chunks_per_row);  // a power of two
-            const int j = c >> sh, e = c & (chunks_per_row - 1);
+            const long j = c >> sh;
+            const int e = (int)(c & (chunks_per_row - 1));
             const long kj = min(k0 + j, total_kept - 1);
             long src = beg + kept_idx[kj];
             src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
