@@ -92,7 +92,7 @@ struct Smem {
     alignas(16) char kv[2 * Tile<HD>::STAGEB];
     int seg_start[ENCODE ? 2 : kMaxSeg + 1];
     int seg_row[ENCODE ? 2 : kMaxSeg];
-    int scan[ENCODE ? 1 : kThreads];
+    int scan[4];  // wave totals of the segment-length scan
 };
 
 // XOR mask of a row's chunk index: for 256-byte rows the two 2-bit halves of
@@ -182,22 +182,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             }
             part += lens[i];
         }
-        sm.scan[tid] = part;
-        __syncthreads();
-        for (int o = 1; o < kThreads; o <<= 1) {
-            const int add = tid >= o ? sm.scan[tid - o] : 0;
-            __syncthreads();
-            sm.scan[tid] += add;
-            __syncthreads();
-        }
-        int run = sm.scan[tid] - part;
+        int run = block4_exclusive_scan(part, sm.scan, &s_vis);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int s = tid * 4 + i;
             if (s < n_seg) sm.seg_start[s] = run;
             run += lens[i];
         }
-        s_vis = sm.scan[kThreads - 1];
         if (tid == 0) sm.seg_start[n_seg] = s_vis;
         __syncthreads();
     }

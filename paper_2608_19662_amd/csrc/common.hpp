@@ -87,4 +87,23 @@ __device__ __forceinline__ float wave_sum(float x) {
     return x;
 }
 
+// Exclusive prefix sum of `part` over the threads of a 4-wave block, in
+// thread order, and the block total: lane shuffles inside each wave, then
+// the four wave totals through `wave_tot` (LDS, 4 ints).  One barrier; every
+// thread of the block must call it.
+__device__ __forceinline__ int block4_exclusive_scan(int part, int* wave_tot, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int incl = part;
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wave_tot[w];
+    *total = wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
+    return before + incl - part;
+}
+
 }  // namespace rc

@@ -59,7 +59,7 @@ template <int HD>
 struct DecSmem {
     int seg_start[kMaxSeg + 1];
     int seg_row[kMaxSeg];
-    int scan[kThreads];
+    int scan[4];  // wave totals of the segment-length scan
     // per wave: two V tile buffers; reused for the cross-wave merge
     alignas(16) char v[4][2][DT<HD>::TILEB];
 };
@@ -89,6 +89,19 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
     const int b = bid / a.n_kv_heads;
     const int R = a.ratio;
 
+    // ---- Q^T (B operand), loaded first since it depends on nothing else:
+    // lane holds head l16 of the group (zero beyond R), dims ks*32 + grp*8 + [0, 8).
+    const int qrow = min(a.cu_q[b], (int)a.lse_rows - 1);
+    bf16x8_t qf[T::NKS];
+#pragma unroll
+    for (int ks = 0; ks < T::NKS; ++ks) {
+        u32x4 w = {0u, 0u, 0u, 0u};
+        if (l16 < R)
+            w = *reinterpret_cast<const u32x4*>(a.q + ((size_t)qrow * a.n_q_heads + g * R + l16) * HD +
+                                                ks * 32 + grp * 8);
+        qf[ks] = __builtin_bit_cast(bf16x8_t, w);
+    }
+
     // ---- visible segments of this (request, layer, group): kept rows of the
     // routed resources, request order.  Exclusive scan of their lengths.
     const size_t e = ((size_t)b * a.n_layers + a.layer) * a.n_kv_heads + g;
@@ -107,16 +120,9 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
         }
         part += lens[i];
     }
-    sm.scan[tid] = part;
-    __syncthreads();
-    for (int o = 1; o < kThreads; o <<= 1) {
-        const int add = tid >= o ? sm.scan[tid - o] : 0;
-        __syncthreads();
-        sm.scan[tid] += add;
-        __syncthreads();
-    }
+    int s_vis;
     {
-        int run = sm.scan[tid] - part;
+        int run = block4_exclusive_scan(part, sm.scan, &s_vis);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int s = tid * 4 + i;
@@ -124,7 +130,6 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
             run += lens[i];
         }
     }
-    const int s_vis = sm.scan[kThreads - 1];
     if (tid == 0) sm.seg_start[n_seg] = s_vis;
     const int c0 = a.cu_ctx[b];
     const int tc = a.cu_ctx[b + 1] - c0;
@@ -161,19 +166,6 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
     int vs_i = 0, vs_hi = seg_hi0, vs_dl = seg_dl0;  // walk for this lane's V keys
     int us_i = 0;                                     // wave-uniform walk (fast test)
     int us_hi = __builtin_amdgcn_readfirstlane(seg_hi0), us_dl = __builtin_amdgcn_readfirstlane(seg_dl0);
-
-    // ---- Q^T (B operand): lane holds head l16 of the group (zero beyond R),
-    // dims ks*32 + grp*8 + [0, 8).
-    const int qrow = min(a.cu_q[b], (int)a.lse_rows - 1);
-    bf16x8_t qf[T::NKS];
-#pragma unroll
-    for (int ks = 0; ks < T::NKS; ++ks) {
-        u32x4 w = {0u, 0u, 0u, 0u};
-        if (l16 < R)
-            w = *reinterpret_cast<const u32x4*>(a.q + ((size_t)qrow * a.n_q_heads + g * R + l16) * HD +
-                                                ks * 32 + grp * 8);
-        qf[ks] = __builtin_bit_cast(bf16x8_t, w);
-    }
 
     // ---- loads of one tile.  K: lane holds key kb*16 + l16 of the tile,
     // dims ks*32 + grp*8 + [0, 8), in registers.  V: copy j of the wave moves
