@@ -15,29 +15,47 @@ namespace rc {
 
 namespace {
 
-// One thread per 16-byte chunk of an output row.  The owning resource of a
-// compacted row is found by binary search over cu_kept.
+// One block per (resource r, KV head g): the kept rows of r for head g go
+// to rows g * total_kept + cu_kept[r] + j of the compacted caches.  Each
+// thread moves U 16-byte chunks per step, all loads issued before the
+// stores; source rows are clamped into the caches.
 __global__ __launch_bounds__(256) void prune_gather_kernel(
-    int chunks_per_row, int n_res, const int32_t* __restrict__ cu_len,
+    int chunks_per_row, int n_kv_heads, const int32_t* __restrict__ cu_len,
     const int32_t* __restrict__ cu_kept, const int32_t* __restrict__ kept_idx, long total_T,
-    long total_kept, long total_chunks, const u32x4* __restrict__ kc, const u32x4* __restrict__ vc,
+    long total_kept, const u32x4* __restrict__ kc, const u32x4* __restrict__ vc,
     u32x4* __restrict__ ko, u32x4* __restrict__ vo) {
-    const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= total_chunks) return;
-    const int c = (int)(idx % chunks_per_row);
-    const long row = idx / chunks_per_row;
-    const long g = row / total_kept;
-    const int j = (int)(row % total_kept);
-    int lo = 0, hi = n_res - 1;  // last r with cu_kept[r] <= j
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (cu_kept[mid] <= j) lo = mid; else hi = mid - 1;
+    constexpr int U = 4;
+    const int r = blockIdx.x / n_kv_heads, g = blockIdx.x % n_kv_heads;
+    const long k0 = cu_kept[r];
+    const long k1 = min((long)cu_kept[r + 1], total_kept);
+    if (k0 < 0 || k1 <= k0) return;
+    const long beg = cu_len[r];
+    const int sh = __builtin_ctz(chunks_per_row);  // a power of two
+    const long n = (k1 - k0) * chunks_per_row;
+    const size_t src_base = (size_t)g * total_T;
+    const size_t dst_base = ((size_t)g * total_kept + k0) * chunks_per_row;
+    for (long c0 = threadIdx.x; c0 < n; c0 += 256 * U) {
+        u32x4 kx[U], vx[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const long c = min(c0 + u * 256, n - 1);
+            const long j = c >> sh;
+            const int e = (int)(c & (chunks_per_row - 1));
+            long src = beg + kept_idx[k0 + j];
+            src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
+            const size_t si = (src_base + src) * chunks_per_row + e;
+            kx[u] = kc[si];
+            vx[u] = vc[si];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const long c = c0 + u * 256;
+            if (c < n) {
+                ko[dst_base + c] = kx[u];
+                vo[dst_base + c] = vx[u];
+            }
+        }
     }
-    long src = (long)cu_len[lo] + kept_idx[j];
-    src = src < 0 ? 0 : (src >= total_T ? total_T - 1 : src);
-    const size_t s = ((size_t)g * total_T + src) * chunks_per_row + c;
-    ko[idx] = kc[s];
-    vo[idx] = vc[s];
 }
 
 // Entry e = (b * L + l) * G + g: count the visible resources and their kept rows.
@@ -219,12 +237,11 @@ hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
                                long total_kept, int n_kv_heads, int head_dim, const void* k_cache,
                                const void* v_cache, void* k_kept, void* v_kept, hipStream_t s) {
     const int cpr = head_dim * elem_bytes / 16;
-    const long total = (long)n_kv_heads * total_kept * cpr;
-    if (total == 0) return hipSuccess;
-    const long blocks = (total + 255) / 256;
+    const long blocks = (long)n_res * n_kv_heads;
+    if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(prune_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr, n_res,
-                       cu_len, cu_kept, kept_idx, total_T, total_kept, total,
+    hipLaunchKernelGGL(prune_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr, n_kv_heads,
+                       cu_len, cu_kept, kept_idx, total_T, total_kept,
                        static_cast<const u32x4*>(k_cache), static_cast<const u32x4*>(v_cache),
                        static_cast<u32x4*>(k_kept), static_cast<u32x4*>(v_kept));
     return hipGetLastError();
