@@ -195,7 +195,6 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
         a.k = static_cast<const uint16_t*>(prefix_k);
         a.v = static_cast<const uint16_t*>(prefix_v);
         a.k_rows = prefix_len;
-    a.k_gstride = prefix_len;
         a.k_gstride = prefix_len;
         a.ck = static_cast<const uint16_t*>(k_cache);
         a.cv = static_cast<const uint16_t*>(v_cache);
