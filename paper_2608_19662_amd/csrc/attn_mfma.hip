@@ -131,12 +131,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     // the q tiles of a (unit, group) come next, so the blocks that run side
     // by side on an XCD stream the same keys through its L2.
     int bid = blockIdx.x;
-    const int g = bid % a.n_kv_heads;
+    int g = bid % a.n_kv_heads;
     bid /= a.n_kv_heads;
     const int jt = a.n_qt - 1 - bid % a.n_qt;
     bid /= a.n_qt;
     const int hq = bid % a.n_hq;
     const int unit = bid / a.n_hq;
+    // Prefill: the group is rotated by the request, so that an XCD serves
+    // every group over the requests rather than one group throughout; routes
+    // give the groups unequal work, and this evens out the XCDs' shares.
+    // The blocks of one (request, group) still share one XCD.
+    if constexpr (!ENCODE) g = (g + unit) % a.n_kv_heads;
 
     int q_len, q_row0, off, stream, pos0 = 0;
     int n_seg = 0, s_vis = 0, ctx_row0 = 0, tc = 0;
