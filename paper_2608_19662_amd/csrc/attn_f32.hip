@@ -62,14 +62,15 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const AttnF32Args a) {
         if (two) {
             // pair (lane, lane + 64), frequency lane
             sincos_rev(rope_revolutions(pos, a.rope.rev[lane]), &s, &c);
-            const float y0 = q0 * c - q1 * s, y1 = q1 * c + q0 * s;
+            // the rounding of the key rotation, written out
+            const float y0 = fmaf(q0, c, -(q1 * s)), y1 = fmaf(q1, c, q0 * s);
             q0 = y0;
             q1 = y1;
         } else {
             // pair (lane, lane + 32), frequency lane % 32
             sincos_rev(rope_revolutions(pos, a.rope.rev[lane & 31]), &s, &c);
             const float partner = __shfl_xor(q0, 32);
-            q0 = (lane < 32) ? q0 * c - partner * s : q0 * c + partner * s;
+            q0 = (lane < 32) ? fmaf(q0, c, -(partner * s)) : fmaf(q0, c, partner * s);
         }
     }
     const float sc = a.scale * 1.44269504088896340736f;

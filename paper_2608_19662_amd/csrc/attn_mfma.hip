@@ -388,8 +388,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                         const float x1 = bf16_bits_to_f32((raw[t][w] >> (16 * h2)) & 0xffffu);
                         const float x2 =
                             bf16_bits_to_f32((raw[t + TL::NT / 2][w] >> (16 * h2)) & 0xffffu);
-                        y1[h2] = x1 * cs2[h2] - x2 * sn2[h2];
-                        y2[h2] = x2 * cs2[h2] + x1 * sn2[h2];
+                        // the rounding of the key rotation, written out
+                        y1[h2] = fmaf(x1, cs2[h2], -(x2 * sn2[h2]));
+                        y2[h2] = fmaf(x2, cs2[h2], x1 * sn2[h2]);
                     }
                     lo[w] = pack_bf16x2(y1[0], y1[1]);
                     hi[w] = pack_bf16x2(y2[0], y2[1]);

@@ -97,8 +97,10 @@ __global__ __launch_bounds__(kThreads) void rope_kernel(const RopeArgs a) {
         for (int e = 0; e < 8; ++e) {
             const float2 k = cs[tk * half + ch * 8 + e];
             const float a1 = x1.get(e), a2 = x2.get(e);
-            y1[e] = a1 * k.x - a2 * k.y;
-            y2[e] = a2 * k.x + a1 * k.y;
+            // one product rounded, the other fused: written out, so that the
+            // rounding does not depend on how the compiler contracts
+            y1[e] = fmaf(a1, k.x, -(a2 * k.y));
+            y2[e] = fmaf(a2, k.x, a1 * k.y);
         }
         x1.set(y1);
         x2.set(y2);
