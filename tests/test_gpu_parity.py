@@ -653,3 +653,65 @@ def test_decode_full_size_over_route_store():
     w = config(5)["attend"]
     run_store_case(w, 11)
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------- seeded random cases
+
+LAYOUTS = [(32, 8, 128), (8, 2, 64), (8, 8, 128), (16, 8, 128), (28, 4, 128), (12, 4, 64),
+           (24, 4, 128), (16, 2, 64), (64, 8, 128), (6, 2, 128), (10, 2, 64)]
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_encode_random_cases(seed):
+    """Seeded random encode problems: head layout, dtype, resource count and
+    lengths (single tokens included), shared prefix and Block positions are
+    all drawn; every output is checked against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    Hq, Hkv, d = LAYOUTS[int(rng.integers(len(LAYOUTS)))]
+    dtype = "f32" if seed % 6 == 5 else "bf16"
+    n = int(rng.integers(1, 9))
+    lengths = np.where(rng.random(n) < 0.2, 1, rng.integers(2, 400, n)).astype(np.int32)
+    P = int(rng.choice([0, 0, 1, 65, 200]))
+    block = P > 0 and rng.random() < 0.5
+    print_case("encode random", seed, Hq, Hkv, d, dtype, lengths.tolist(), P, block)
+    w = EncodeWorkload(seed=2000 + seed, lengths=lengths, n_q_heads=Hq, n_kv_heads=Hkv,
+                       head_dim=d, dtype=dtype, rope_base=1e6 if seed % 2 else 1e4)
+    q, k, v = w.tensors("cpu")
+    kw, okw = {}, {}
+    if P:
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        pk, pv = prefix_cache(3000 + seed, P, Hkv, d, tdt, w.rope_base)
+        pb = (P + w.cu_len[:-1] if block else np.full(n, P)).astype(np.int32)
+        kw = dict(pos_base=pb, prefix_k=pk, prefix_v=pv)
+        okw = dict(pos_base=pb, prefix_k=pk.cpu(), prefix_v=pv.cpu())
+    out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV), **kw)
+    ref = oracle.encode(q, k, v, w.cu_len, w.rope_base, **okw)
+    check(out, ref["out"], dtype, "out")
+    check(kc, ref["k_cache"], "f32" if dtype == "f32" else "bf16-ulp", "k_cache")
+    check(lse, ref["lse"], dtype, "lse")
+    assert torch.equal(vc.cpu(), v.permute(1, 0, 2).contiguous())
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_attend_random_cases(seed):
+    """Seeded random attend problems: prefill or decode, request count, query
+    and context lengths, resource pool and requests' resource lists (empty
+    ones included), route density, pruning, and whether the kept rows come
+    from a GPU prune of the full caches; checked against the oracle."""
+    rng = np.random.default_rng(4000 + seed)
+    Hq, Hkv, d = LAYOUTS[int(rng.integers(len(LAYOUTS)))]
+    dtype = "f32" if seed % 6 == 5 else "bf16"
+    n_req = int(rng.integers(1, 5))
+    pool = int(rng.integers(1, 9))
+    decode = seed % 2 == 1
+    q_lens = np.ones(n_req, np.int32) if decode else rng.integers(1, 200, n_req).astype(np.int32)
+    ctx_lens = (q_lens + rng.integers(0, 500, n_req)).astype(np.int32)
+    mask_p = float(rng.choice([0.0, 0.25, 0.5, 1.0]))
+    prune = bool(rng.random() < 0.6)
+    chain = prune and bool(rng.random() < 0.5)
+    print_case("attend random", seed, Hq, Hkv, d, dtype, q_lens.tolist(), ctx_lens.tolist(), pool,
+               mask_p, prune, chain)
+    w = small_attend(5000 + seed, n_req, pool, Hq, Hkv, d, dtype, q_lens, ctx_lens, L=2,
+                     prune=prune, mask_p=mask_p if mask_p < 1 else 2.0,
+                     max_len=int(rng.integers(1, 600)))
+    run_attend_case(w, int(rng.integers(2)), chain=chain)
