@@ -715,3 +715,61 @@ def test_attend_random_cases(seed):
                      prune=prune, mask_p=mask_p if mask_p < 1 else 2.0,
                      max_len=int(rng.integers(1, 600)))
     run_attend_case(w, int(rng.integers(2)), chain=chain)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_index_random_cases(seed):
+    """Seeded random structures for the index work, all bit-exact against the
+    oracle: kept-row gather, route lists (requests with no resources
+    included) and the route-compacted store of every layer."""
+    rng = np.random.default_rng(6000 + seed)
+    n_res = int(rng.integers(1, 41))
+    G = int(rng.choice([1, 2, 4, 8]))
+    L = int(rng.integers(1, 5))
+    d = int(rng.choice([64, 128]))
+    dt = torch.float32 if seed % 4 == 3 else torch.bfloat16
+    lengths = np.where(rng.random(n_res) < 0.2, 1, rng.integers(2, 500, n_res)).astype(np.int32)
+    cu_len = prefix(lengths)
+    cu_kept, kept_idx = draw_kept(rng, lengths, float(rng.choice([0.05, 0.3, 1.0])))
+    mask = (rng.random((n_res, L, G)) < float(rng.choice([0.0, 0.25, 0.7, 1.0]))).astype(np.uint8)
+    n_req = int(rng.integers(1, 7))
+    reqs = [rng.permutation(n_res)[: rng.integers(0, n_res + 1)] for _ in range(n_req)]
+    print_case("index random", seed, n_res, G, L, d, dt, n_req)
+    T, K = int(cu_len[-1]), int(cu_kept[-1])
+    kc = normal((G, T, d), dt, 7000 + seed, 1, DEV)
+    vc = normal((G, T, d), dt, 7000 + seed, 2, DEV)
+    # kept-row gather
+    kk = torch.empty(G, K, d, dtype=dt, device=DEV)
+    vk = torch.empty_like(kk)
+    rc.prune_gather(kc, vc, i32(cu_len), i32(cu_kept), i32(kept_idx), kk, vk)
+    rk, rv = oracle.prune(kc.cpu(), vc.cpu(), cu_len, cu_kept, kept_idx)
+    assert np.array_equal(oracle.host_view(kk.cpu()), rk)
+    assert np.array_equal(oracle.host_view(vk.cpu()), rv)
+    # route lists
+    req_res_off = prefix([len(r) for r in reqs])
+    req_res = np.concatenate(reqs).astype(np.int32) if req_res_off[-1] else np.zeros(0, np.int32)
+    mask_d = torch.from_numpy(mask).to(DEV)
+    E = n_req * L * G
+    route_off = torch.empty(E + 1, dtype=torch.int32, device=DEV)
+    route_res = torch.empty(max(1, len(req_res) * L * G), dtype=torch.int32, device=DEV)
+    route_tokens = torch.empty(E, dtype=torch.int32, device=DEV)
+    rc.build_routes(i32(req_res_off), i32(req_res if len(req_res) else [0]), mask_d, i32(cu_kept),
+                    route_off, route_res, route_tokens)
+    off, res, tok = oracle.routes(req_res_off, req_res, mask, cu_kept)
+    assert np.array_equal(route_off.cpu().numpy(), off)
+    assert np.array_equal(route_res.cpu().numpy()[: off[-1]], res)
+    assert np.array_equal(route_tokens.cpu().numpy(), tok)
+    # route-compacted store, every layer
+    st = torch.empty(L, n_res * G + 1, dtype=torch.int32, device=DEV)
+    rc.route_store_offsets(mask_d, i32(cu_kept), st, total_kept=K)
+    st_h = st.cpu().numpy()
+    assert np.array_equal(st_h, oracle.store_offsets(mask, cu_kept))
+    for layer in range(L):
+        rows = int(st_h[layer, -1])
+        ks = torch.empty(rows, d, dtype=dt, device=DEV)
+        vs = torch.empty_like(ks)
+        rc.store_routes(kc, vc, i32(cu_len), i32(cu_kept), i32(kept_idx), st, layer, ks, vs,
+                        total_kept=K)
+        rk, rv = oracle.store_routes(kc.cpu(), vc.cpu(), cu_len, cu_kept, kept_idx, mask, layer)
+        assert np.array_equal(oracle.host_view(ks.cpu()), rk)
+        assert np.array_equal(oracle.host_view(vs.cpu()), rv)
