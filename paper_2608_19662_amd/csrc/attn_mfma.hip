@@ -567,21 +567,38 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
 
     const float l = pair_sum(lsum);
-    if (my_q < q_len && q_row0 + my_q < a.lse_rows) {
+    // Output through LDS: each wave writes its 32 normalised rows there
+    // (16-byte chunks swizzled by row), then stores whole rows with 16-byte
+    // stores, so every store instruction fills complete lines.
+    __syncthreads();  // every wave is done with the K / V stages
+    {
+        constexpr int CPR = TL::CPR;
+        char* ob = lds + wave * 32 * ROWB;
         const float inv = 1.0f / l;
-        uint16_t* orow = a.out + ((size_t)(q_row0 + my_q) * a.n_q_heads + head) * HD;
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
-                const int d = db * 32 + r4 * 8 + half * 4;
+                const int c = db * 4 + r4;  // 16-byte chunk of the row
                 const uint2 w = make_uint2(pack_bf16x2(oacc[db][r4 * 4 + 0] * inv, oacc[db][r4 * 4 + 1] * inv),
                                            pack_bf16x2(oacc[db][r4 * 4 + 2] * inv, oacc[db][r4 * 4 + 3] * inv));
-                *reinterpret_cast<uint2*>(orow + d) = w;
+                *reinterpret_cast<uint2*>(ob + l32 * ROWB + ((c ^ (l32 % CPR)) << 4) + half * 8) = w;
             }
-        if (a.lse && half == 0)
-            a.lse[(size_t)head * a.lse_rows + q_row0 + my_q] = m * sl2 * 0.69314718055994531f + logf(l);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        __builtin_amdgcn_wave_barrier();
+        constexpr int RPS = 64 / CPR;  // rows per store instruction
+        const int q_base = q_first + (wave / a.hpw) * 32;
+#pragma unroll
+        for (int it = 0; it < 32 / RPS; ++it) {
+            const int r = it * RPS + lane / CPR, c = lane % CPR;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(ob + r * ROWB + ((c ^ (r % CPR)) << 4));
+            const int q = q_base + r;
+            if (q < q_len && q_row0 + q < a.lse_rows)
+                *reinterpret_cast<u32x4*>(a.out + ((size_t)(q_row0 + q) * a.n_q_heads + head) * HD + c * 8) = v;
+        }
     }
+    if (a.lse && half == 0 && my_q < q_len && q_row0 + my_q < a.lse_rows)
+        a.lse[(size_t)head * a.lse_rows + q_row0 + my_q] = m * sl2 * 0.69314718055994531f + logf(l);
 }
 
 }  // namespace
