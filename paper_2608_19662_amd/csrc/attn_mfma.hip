@@ -123,7 +123,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     char* lds = sm.kv;
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: a scalar
     const int l32 = lane & 31, half = lane >> 5;
 
     // block -> (unit, head slice, q tile [longest first], group).  The group
@@ -445,11 +446,13 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     __syncthreads();  // every wave has read K(0) before K(2) is copied over it
 
     const float sl2 = a.scale_log2;
-    const float lazy = 8.0f / sl2;
+    const float lazy = a.lazy;
     const bf16x2 ones2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0) in bf16
     float m = -INFINITY;   // running max of raw logits for this lane's row
     float lsum = 0.f;      // this lane's partial sum of the (bf16-rounded) weights
-    const int lim = off + my_q;  // keys p <= lim are visible to this lane's row
+    // keys p <= off + my_q are visible to this lane's row; this lane's S^T
+    // entries of a tile start at key offset half * 4
+    const int lim4 = off + my_q - half * 4;
     f32x16 oacc[TL::NDB];
 #pragma unroll
     for (int db = 0; db < TL::NDB; ++db) oacc[db] = f32x16{};
@@ -467,7 +470,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         f32x16* sc = sacc[cur];
         // causal / stream-end mask, only on tiles that reach past the first row's limit
         if (kt * kBK + kBK - 1 > off + q_first) {
-            const int rem = lim - kt * kBK - half * 4;  // key offsets above rem are masked
+            const int rem = lim4 - kt * kBK;  // key offsets above rem are masked
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -572,6 +575,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     // stores, so every store instruction fills complete lines.
     __syncthreads();  // every wave is done with the K / V stages
     {
+        // lane-derived values again, from the lane counter rather than kept
+        // in registers across the loop
+        const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+        const int row = ln & 31, hf = ln >> 5;  // this lane's row, and which half of it
         constexpr int CPR = TL::CPR;
         char* ob = lds + wave * 32 * ROWB;
         const float inv = 1.0f / l;
@@ -582,7 +589,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
                 const int c = db * 4 + r4;  // 16-byte chunk of the row
                 const uint2 w = make_uint2(pack_bf16x2(oacc[db][r4 * 4 + 0] * inv, oacc[db][r4 * 4 + 1] * inv),
                                            pack_bf16x2(oacc[db][r4 * 4 + 2] * inv, oacc[db][r4 * 4 + 3] * inv));
-                *reinterpret_cast<uint2*>(ob + l32 * ROWB + ((c ^ (l32 % CPR)) << 4) + half * 8) = w;
+                *reinterpret_cast<uint2*>(ob + row * ROWB + ((c ^ (row % CPR)) << 4) + hf * 8) = w;
             }
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
         __builtin_amdgcn_wave_barrier();
@@ -590,15 +597,16 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         const int q_base = q_first + (wave / a.hpw) * 32;
 #pragma unroll
         for (int it = 0; it < 32 / RPS; ++it) {
-            const int r = it * RPS + lane / CPR, c = lane % CPR;
+            const int r = it * RPS + ln / CPR, c = ln % CPR;
             const u32x4 v = *reinterpret_cast<const u32x4*>(ob + r * ROWB + ((c ^ (r % CPR)) << 4));
             const int q = q_base + r;
             if (q < q_len && q_row0 + q < a.lse_rows)
                 *reinterpret_cast<u32x4*>(a.out + ((size_t)(q_row0 + q) * a.n_q_heads + head) * HD + c * 8) = v;
         }
+        const int q = q_base + row;
+        if (a.lse && hf == 0 && q < q_len && q_row0 + q < a.lse_rows)
+            a.lse[(size_t)head * a.lse_rows + q_row0 + q] = m * sl2 * 0.69314718055994531f + logf(l);
     }
-    if (a.lse && half == 0 && my_q < q_len && q_row0 + my_q < a.lse_rows)
-        a.lse[(size_t)head * a.lse_rows + q_row0 + my_q] = m * sl2 * 0.69314718055994531f + logf(l);
 }
 
 }  // namespace
@@ -609,12 +617,14 @@ hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStr
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
     if (a.hpw * a.rbw != 4) return hipErrorInvalidValue;  // one (head, row block) pair per wave
     dim3 grid((unsigned)blocks), block(kThreads);
+    AttnArgs b = a;
+    b.lazy = 8.0f / a.scale_log2;
     if (head_dim == 128) {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, a);
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, b);
+        else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, b);
     } else {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, a);
-        else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, a);
+        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, b);
+        else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, b);
     }
     return hipGetLastError();
 }
