@@ -34,6 +34,11 @@
 // in the key order in which the S^T accumulator hands P^T to the second
 // product.
 //
+// Output.  The normalised rows go through LDS and leave as whole rows, four
+// 256-byte rows per 16-byte store instruction.  Values the loop does not use
+// (the lane index, the rescale threshold) are not held across it, so that the
+// registers spilled around the last tiles stay few.
+//
 // Tiles never cross a resource boundary in encode, and the reduction order
 // depends only on local indices, so a resource's outputs are bit-identical
 // wherever it is packed and whatever its neighbours are.
