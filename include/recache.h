@@ -97,9 +97,14 @@ int recache_rope_q(int dtype, int T, int n_heads, int head_dim, double rope_base
  * Rotate k[T][n_kv_heads][head_dim] at pos[T] and write it to
  * k_cache[g][row0 + t][:]; copy v[T][n_kv_heads][head_dim] to
  * v_cache[g][row0 + t][:].  Caches are [n_kv_heads][cache_rows][head_dim];
- * requires 0 <= row0 and row0 + T <= cache_rows.  Used to append conversation
- * K/V (context positions) and, inside recache_encode_resources, resource K/V
- * at resource-local positions.
+ * requires 0 <= row0 and row0 + T <= cache_rows.  This is the cache
+ * construction step of Sec. 3, "Resource-Wise Attention": each resource's
+ * keys are rotated at local indices assigned while its cache is built
+ * (pos = j for token j), and the surrounding context keeps its original
+ * positions (pass them in pos).  Used to append conversation K/V and, inside
+ * recache_encode_resources, resource K/V at resource-local positions.
+ * Errors: RECACHE_EINVAL for T < 0, rows outside the cache, a null pointer or
+ * rope_base <= 1; RECACHE_EUNSUPPORTED for dtype / head_dim.
  */
 int recache_rope_kv(int dtype, int T, int n_kv_heads, int head_dim, double rope_base,
                     const int32_t* pos, const void* k, const void* v,
@@ -109,7 +114,9 @@ int recache_rope_kv(int dtype, int T, int n_kv_heads, int head_dim, double rope_
  * One layer of resource encoding (Sec. 3, "Resource-Wise Attention";
  * Fig. 2(a)).  n_res resources are packed in order: resource r owns rows
  * [cu_len[r], cu_len[r+1]) (device int32, cu_len[0] = 0, every length >= 1,
- * cu_len[n_res] = total_T, every length <= max_len).  Token j of resource r
+ * cu_len[n_res] = total_T, every length <= max_len: see
+ * recache_check_encode_lengths; a resource longer than max_len gets NaN rows
+ * instead of outputs).  Token j of resource r
  * gets position pos_base[r] + j (pos_base device int32 [n_res], or NULL for
  * 0: resource-local positions, pos(t_ij) = j).
  *
@@ -230,9 +237,14 @@ int recache_store_routes(int dtype, int layer, int n_layers, int n_res, const in
 
 /*
  * Workspace bytes that recache_attend_cached needs for these sizes (0 when
- * max_q > 1: the prefill kernels use none).  max_kv is an upper bound on the
- * keys a (request, group) can see in one layer (route tokens + context), used
- * only to size the split-KV decode; 0 means "use max_ctx".
+ * max_q > 1: the prefill kernels use none).  Library convention, not a
+ * passage of the paper: decode (Fig. 2's final mask with one query per
+ * request) splits each (request, group) key stream into chunks whose partial
+ * outputs and log-sum-exps are merged afterwards; the workspace holds those
+ * partials, fp32, n_req * n_q_heads * splits * (head_dim + 2) values.
+ * max_kv is an upper bound on the keys a (request, group) can see in one layer
+ * (route tokens + context), used only to choose the split count; 0 means
+ * "use max_ctx".  Returns 0 for invalid sizes.  Pure host arithmetic.
  */
 size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max_kv,
                                       int n_q_heads, int n_kv_heads, int head_dim);
@@ -265,7 +277,12 @@ size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max
  *   route_off/route_res/route_tokens: output of recache_build_routes
  *   out[total_q][n_q_heads][head_dim]; lse[n_q_heads][total_q] or NULL
  *   max_route_len: upper bound on the resources of any route list (at most
- *       1024), i.e. on resources per request
+ *       1024), i.e. on resources per request (check the request lists with
+ *       recache_check_requests); a route list longer than 1024 makes the
+ *       kernels write NaN for that (request, group) instead of truncating it
+ *   Tq_b must also not exceed max_q: the prefill grid is sized by it, and
+ *       rows past it are written as NaN; with max_q = 1 every request must
+ *       have exactly one query (decode writes NaN for one that has more)
  *   workspace: device scratch of recache_attend_workspace_bytes(...) bytes
  *       (may be NULL when that is 0); contents need no initialisation.
  */
@@ -300,16 +317,37 @@ int recache_select_routes(int n_layers, int n_groups, const double* s_layer, con
                           double* w_group, double* rho, double* cc_layer, double* cc_group);
 
 /*
- * [host] Validators for host copies of index arrays.  Return RECACHE_OK or
- * RECACHE_EINVAL (with recache_last_error() naming the first bad entry).
+ * [host] Validators for host copies of index arrays.  The device kernels trust
+ * the index arrays they are given (library convention: validation is a host
+ * step, so a kernel never waits on an error check), and these functions state
+ * the preconditions the problem statement of Sec. 3 puts on them: X is a
+ * sequence of resources R_i of D_i >= 1 tokens packed in order, each request
+ * lists the resources it retrieved, and a semantically pruned resource keeps
+ * a non-empty subsequence of its own tokens ("Semantic Pruning").  Each
+ * returns RECACHE_OK or RECACHE_EINVAL (recache_last_error() names the first
+ * bad entry); none touches device memory.
  *   recache_check_offsets: cu[0] = 0, cu non-decreasing (strictly increasing
  *       when strict != 0), cu[n] = total.
  *   recache_check_kept: for each resource, kept indices strictly ascending,
  *       inside [0, D_r), at least one, and cu_kept consistent.
+ *   recache_check_encode_lengths: the packing offsets of an encode call
+ *       (strictly increasing from 0 to total_T) with every resource at most
+ *       max_len tokens long.  The encode grid is sized by max_len; a longer
+ *       resource would reach past it (the kernels then write NaN into that
+ *       resource's rows rather than leave them unwritten).
+ *   recache_check_requests: the request lists of recache_build_routes
+ *       (req_res_off from 0, non-decreasing, req_res_off[n_req] =
+ *       total_req_res; every id in [0, n_res)) with no request listing more
+ *       than max_route_len resources, and max_route_len <= 1024, the longest
+ *       route list the attention kernels take (a longer list makes them write
+ *       NaN outputs for that route rather than drop resources).
  */
 int recache_check_offsets(const int32_t* cu, int n, int total, int strict);
 int recache_check_kept(const int32_t* cu_len, const int32_t* cu_kept, const int32_t* kept_idx,
                        int n_res);
+int recache_check_encode_lengths(const int32_t* cu_len, int n_res, int total_T, int max_len);
+int recache_check_requests(const int32_t* req_res_off, const int32_t* req_res, int n_req,
+                           int total_req_res, int n_res, int max_route_len);
 
 #ifdef __cplusplus
 }

@@ -380,15 +380,19 @@ size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max
     return decode_workspace_bytes(n_req, n_q_heads, head_dim, decode_splits(n_req, n_kv_heads, kv));
 }
 
-int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const int32_t* cu_q,
-                          const int32_t* cu_ctx, int total_q, int max_q, int max_ctx, int max_kv,
-                          int max_route_len, int n_q_heads, int n_kv_heads, int head_dim,
-                          float softmax_scale, const void* q, const void* ctx_k,
-                          const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
-                          int res_rows, const int32_t* cu_kept, const int32_t* res_off,
-                          const int32_t* route_off, const int32_t* route_res,
-                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Scalar and pointer checks of an attend call (everything but the
+// workspace); no HIP call.
+int check_attend(int dtype, int layer, int n_layers, int n_req, const int32_t* cu_q,
+                 const int32_t* cu_ctx, int total_q, int max_q, int max_ctx, int max_route_len,
+                 int n_q_heads, int n_kv_heads, int head_dim, float softmax_scale, const void* q,
+                 const void* ctx_k, const void* ctx_v, int ctx_rows, const void* res_k,
+                 const void* res_v, int res_rows, const int32_t* cu_kept, const int32_t* res_off,
+                 const int32_t* route_off, const int32_t* route_res, const int32_t* route_tokens,
+                 const void* out) {
     int rc_ = check_dtype_dim(dtype, head_dim);
     if (rc_) return rc_;
     if ((rc_ = check_heads(dtype, n_q_heads, n_kv_heads))) return rc_;
@@ -410,6 +414,27 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                 cu_kept && route_off && route_res && route_tokens && out,
             RECACHE_EINVAL, "null pointer argument");
     REQUIRE(!(isnan(softmax_scale) || isinf(softmax_scale)), RECACHE_EINVAL, "softmax_scale not finite");
+    return RECACHE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const int32_t* cu_q,
+                          const int32_t* cu_ctx, int total_q, int max_q, int max_ctx, int max_kv,
+                          int max_route_len, int n_q_heads, int n_kv_heads, int head_dim,
+                          float softmax_scale, const void* q, const void* ctx_k,
+                          const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
+                          int res_rows, const int32_t* cu_kept, const int32_t* res_off,
+                          const int32_t* route_off, const int32_t* route_res,
+                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    int rc_ = check_attend(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q, max_ctx,
+                           max_route_len, n_q_heads, n_kv_heads, head_dim, softmax_scale, q, ctx_k,
+                           ctx_v, ctx_rows, res_k, res_v, res_rows, cu_kept, res_off, route_off,
+                           route_res, route_tokens, out);
+    if (rc_) return rc_;
     const float scale = resolve_scale(softmax_scale, head_dim);
     const int ratio = n_q_heads / n_kv_heads;
     const hipStream_t s = as_stream(stream);
@@ -540,6 +565,36 @@ int recache_check_kept(const int32_t* cu_len, const int32_t* cu_kept, const int3
                     j - 1, kept_idx[j - 1], r);
         }
     }
+    return ok();
+}
+
+int recache_check_encode_lengths(const int32_t* cu_len, int n_res, int total_T, int max_len) {
+    REQUIRE(cu_len && n_res >= 1, RECACHE_EINVAL, "null offsets or n_res < 1");
+    int rc_ = recache_check_offsets(cu_len, n_res, total_T, 1);
+    if (rc_) return rc_;
+    for (int r = 0; r < n_res; ++r)
+        REQUIRE(cu_len[r + 1] - cu_len[r] <= max_len, RECACHE_EINVAL,
+                "resource %d has %d tokens, more than max_len %d", r, cu_len[r + 1] - cu_len[r],
+                max_len);
+    return ok();
+}
+
+int recache_check_requests(const int32_t* req_res_off, const int32_t* req_res, int n_req,
+                           int total_req_res, int n_res, int max_route_len) {
+    REQUIRE(req_res_off && n_req >= 1 && n_res >= 1, RECACHE_EINVAL,
+            "null request offsets, n_req < 1 or n_res < 1");
+    REQUIRE(total_req_res == 0 || req_res, RECACHE_EINVAL, "null request lists");
+    REQUIRE(max_route_len >= 0 && max_route_len <= 1024, RECACHE_EINVAL,
+            "max_route_len %d outside [0, 1024]", max_route_len);
+    int rc_ = recache_check_offsets(req_res_off, n_req, total_req_res, 0);
+    if (rc_) return rc_;
+    for (int b = 0; b < n_req; ++b)
+        REQUIRE(req_res_off[b + 1] - req_res_off[b] <= max_route_len, RECACHE_EINVAL,
+                "request %d lists %d resources, more than max_route_len %d", b,
+                req_res_off[b + 1] - req_res_off[b], max_route_len);
+    for (int j = 0; j < total_req_res; ++j)
+        REQUIRE(req_res[j] >= 0 && req_res[j] < n_res, RECACHE_EINVAL,
+                "req_res[%d] = %d outside [0, %d)", j, req_res[j], n_res);
     return ok();
 }
 

@@ -51,6 +51,16 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const AttnF32Args a) {
         q_row0 = a.cu_q[unit];
         q_len = a.cu_q[unit + 1] - q_row0;
     }
+    if (row == a.max_rows - 1 && q_len > a.max_rows) {
+        // rows past the grid's max_rows: NaN, so that a caller's size error
+        // shows in the outputs instead of leaving them unwritten
+        for (int r = a.max_rows; r < q_len && (long)q_row0 + r < a.lse_rows; ++r) {
+            float* op = a.out + ((size_t)(q_row0 + r) * a.n_q_heads + head) * a.head_dim;
+            op[lane] = __builtin_nanf("");
+            if (a.head_dim == 128) op[lane + 64] = __builtin_nanf("");
+            if (a.lse && lane == 0) a.lse[(size_t)head * a.lse_rows + q_row0 + r] = __builtin_nanf("");
+        }
+    }
     if (row >= q_len || q_row0 + row >= a.lse_rows) return;
 
     const float* qp = a.q + ((size_t)(q_row0 + row) * a.n_q_heads + head) * d;

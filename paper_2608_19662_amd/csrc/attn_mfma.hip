@@ -120,6 +120,29 @@ __device__ __forceinline__ void wait_vm0() {
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt / lgkmcnt unconstrained
 }
 
+// Rows a block is responsible for but cannot compute (its route list is
+// longer than the segment table, or they lie past the query rows the grid
+// was sized for): NaN in out and lse, so that a caller's size error shows in
+// the outputs instead of leaving rows unwritten or dropping resources.
+// Rows [r_begin, r_end) of unit rows starting at q_row0, heads
+// [head0, head0 + n_heads).
+template <int HD>
+__device__ __forceinline__ void poison_rows(const AttnArgs& a, int head0, int n_heads, int q_row0,
+                                         int r_begin, int r_end) {
+    constexpr int CPR = HD / 8;
+    const u32x4 nan8 = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};  // bf16 NaNs
+    const long n = (long)max(r_end - r_begin, 0) * n_heads * CPR;
+    for (long i = threadIdx.x; i < n; i += kThreads) {
+        const int c = (int)(i % CPR);
+        const long rest = i / CPR;
+        const int h = head0 + (int)(rest % n_heads);
+        const long row = (long)q_row0 + r_begin + rest / n_heads;
+        if (row < 0 || row >= a.lse_rows) continue;
+        *reinterpret_cast<u32x4*>(a.out + ((size_t)row * a.n_q_heads + h) * HD + c * 8) = nan8;
+        if (c == 0 && a.lse) a.lse[(size_t)h * a.lse_rows + row] = __builtin_nanf("");
+    }
+}
+
 template <int HD, bool ENCODE>
 __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a) {
     using TL = Tile<HD>;
@@ -170,6 +193,12 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
     const int wg_rows = 32 * a.rbw;
     const int q_first = jt * wg_rows;
+    // the grid covers query rows [0, n_qt * wg_rows) of every unit; the block
+    // of the last tile answers for any rows beyond
+    if (jt == a.n_qt - 1 && q_len > a.n_qt * wg_rows) {
+        poison_rows<HD>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_len);
+        return;
+    }
     if (q_first >= q_len) return;
     const int q_last = min(q_first + wg_rows, q_len) - 1;
 
@@ -178,7 +207,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         // routed resources, request order.  Exclusive scan of their lengths.
         const size_t e = ((size_t)unit * a.n_layers + a.layer) * a.n_kv_heads + g;
         const int r0 = a.route_off[e];
-        n_seg = min(a.route_off[e + 1] - r0, kMaxSeg);
+        n_seg = a.route_off[e + 1] - r0;
+        if (n_seg > kMaxSeg) {
+            poison_rows<HD>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_last + 1);
+            return;
+        }
         int part = 0;
         int lens[4];
 #pragma unroll

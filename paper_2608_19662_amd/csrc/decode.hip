@@ -106,7 +106,22 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
     // routed resources, request order.  Exclusive scan of their lengths.
     const size_t e = ((size_t)b * a.n_layers + a.layer) * a.n_kv_heads + g;
     const int r0 = a.route_off[e];
-    const int n_seg = min(a.route_off[e + 1] - r0, kMaxSeg);
+    const int n_seg = a.route_off[e + 1] - r0;
+    if (n_seg > kMaxSeg || a.cu_q[b + 1] - a.cu_q[b] != 1) {
+        // A route list longer than the segment table, or a request that does
+        // not have exactly one query: this split's partial becomes NaN with
+        // an infinite max, which the merge turns into NaN outputs for the
+        // group (a caller's size error shows instead of dropped keys).
+        for (int idx = tid; idx < R * HD; idx += kThreads) {
+            const size_t slot = ((size_t)b * a.n_q_heads + g * R + idx / HD) * a.n_splits + split;
+            a.ws_o[slot * HD + idx % HD] = __builtin_nanf("");
+            if (idx % HD == 0) {
+                a.ws_ml[slot * 2 + 0] = INFINITY;
+                a.ws_ml[slot * 2 + 1] = __builtin_nanf("");
+            }
+        }
+        return;
+    }
     int lens[4], part = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {

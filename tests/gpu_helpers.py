@@ -13,6 +13,12 @@ Tolerances (stated once, used by every GPU test):
                 plus the absolute error of the fp32 rotation before rounding:
                 <= 2^-7 |oracle| + 1e-5 (the absolute term matters where the
                 two products of a rotation cancel).
+  LSE (fp32 outputs of bf16 calls): |gpu - oracle| <= 1e-2 absolute.  The
+                LSE is never rounded to bf16; what moves it is the row sum of
+                the bf16-rounded weights the kernels normalise by (each weight
+                within 2^-9 relative, so ln of the sum within about 2^-9) and
+                fp32 arithmetic (|lse| ~ 10 gives ~1e-6), far inside 1e-2.
+                fp32 calls keep the 1e-5 bar for the LSE too.
   index work:   bit-exact.
 """
 from __future__ import annotations
@@ -33,6 +39,11 @@ def f64(t) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+def lse_rule(dtype: str) -> str:
+    """Tolerance rule of an LSE output for a call in dtype ("f32" or "bf16")."""
+    return "f32" if dtype == "f32" else "lse"
+
+
 def check(gpu, ref, dtype: str, name: str):
     """Assert the tolerance rule; returns the max abs error."""
     g = f64(gpu)
@@ -41,6 +52,8 @@ def check(gpu, ref, dtype: str, name: str):
     err = np.abs(g - ref)
     if dtype == "f32":
         bound = np.full_like(ref, 1e-5)
+    elif dtype == "lse":
+        bound = np.full_like(ref, 1e-2)
     elif dtype == "bf16-ulp":
         bound = 2.0 ** -7 * np.abs(ref) + 1e-5
     else:

@@ -179,3 +179,64 @@ def test_python_binding_refuses_host_tensors():
     x = torch.zeros(4, 2, 64)
     with pytest.raises(TypeError):
         rc.rope_q(x, torch.zeros(4, dtype=torch.int32), 1e4)
+
+
+def test_check_encode_lengths():
+    rc.check_encode_lengths([0, 3, 5, 9], 4)
+    for cu, max_len in [([0, 3, 5, 9], 3),      # a resource of 4 tokens, max_len 3
+                        ([0, 3, 3, 9], 6),      # an empty resource
+                        ([1, 3], 5)]:           # offsets not from 0
+        with pytest.raises(rc.RecacheError) as e:
+            rc.check_encode_lengths(cu, max_len)
+        assert e.value.code == rc.EINVAL
+        assert rc.last_error()
+
+
+def test_check_requests():
+    rc.check_requests([0, 2, 2, 5], [1, 0, 3, 2, 1], 4, 3)
+    rc.check_requests([0, 0], [], 4, 0)           # a request with no resources
+    for off, res, n_res, bound in [([0, 2, 2, 5], [1, 0, 3, 2, 1], 4, 2),  # 3 listed, bound 2
+                                   ([0, 2], [0, 4], 4, 8),                 # id outside [0, 4)
+                                   ([0, 2], [0, 1], 4, 1025),              # over the 1024 limit
+                                   ([0, 3, 2], [0, 1, 2], 4, 8)]:          # decreasing offsets
+        with pytest.raises(rc.RecacheError) as e:
+            rc.check_requests(off, res, n_res, bound)
+        assert e.value.code == rc.EINVAL
+    assert rc.route_len_bound([0, 2, 2, 5]) == 3
+
+
+def test_python_binding_checks_shapes_first():
+    """Every tensor's shape is checked against the call's sizes before any
+    device pointer is taken (a buffer smaller than the sizes passed on would
+    become an access outside it); host tensors of the right shapes are then
+    refused as host memory."""
+    torch = pytest.importorskip("torch")
+    bf = torch.bfloat16
+    z = lambda *s, dt=bf: torch.zeros(*s, dtype=dt)
+    i = lambda n: torch.zeros(n, dtype=torch.int32)
+    T, Hq, Hkv, d = 10, 8, 2, 64
+    good = dict(q=z(T, Hq, d), k=z(T, Hkv, d), v=z(T, Hkv, d), cu_len=i(3), max_len=6,
+                rope_base=1e6, out=z(T, Hq, d), k_cache=z(Hkv, T, d), v_cache=z(Hkv, T, d),
+                lse=z(Hq, T, dt=torch.float32))
+    for key, bad in [("out", z(T - 1, Hq, d)), ("k_cache", z(Hkv, T + 1, d)),
+                     ("v", z(T, Hkv + 1, d)), ("lse", z(Hq, T - 1, dt=torch.float32))]:
+        with pytest.raises(ValueError):
+            rc.encode_resources(**dict(good, **{key: bad}))
+    with pytest.raises(TypeError):
+        rc.encode_resources(**good)
+    n_req, L = 2, 3
+    E = n_req * L * Hkv
+    ga = dict(q=z(4, Hq, d), ctx_k=z(Hkv, 9, d), ctx_v=z(Hkv, 9, d), cu_q=i(n_req + 1),
+              cu_ctx=i(n_req + 1), max_q=2, max_ctx=5, res_k=z(Hkv, 7, d), res_v=z(Hkv, 7, d),
+              cu_kept=i(4), route_off=i(E + 1), route_res=i(30), route_tokens=i(E), layer=0,
+              n_layers=L, out=z(4, Hq, d), max_route_len=3)
+    for key, bad in [("out", z(5, Hq, d)), ("route_off", i(E)), ("route_tokens", i(E + 1)),
+                     ("res_v", z(Hkv, 6, d)), ("ctx_v", z(Hkv, 8, d)), ("cu_ctx", i(n_req))]:
+        with pytest.raises(ValueError):
+            rc.attend_cached(**dict(ga, **{key: bad}))
+    with pytest.raises(ValueError):  # a store table row of the wrong length
+        rc.attend_cached(**dict(ga, res_k=z(7, d), res_v=z(7, d), res_off=i(3 * Hkv)))
+    with pytest.raises(TypeError):  # max_route_len has no default
+        rc.attend_cached(**{k: v for k, v in ga.items() if k != "max_route_len"})
+    with pytest.raises(TypeError):
+        rc.attend_cached(**ga)
