@@ -297,6 +297,40 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           size_t workspace_bytes, void* stream);
 
 /*
+ * recache_attend_cached for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The same arguments and the same results (the same kernels)
+ * without workspace / workspace_bytes: decode keeps its split partials in a
+ * static device array of the library, RECACHE_NOALLOC_SCRATCH_BYTES (32 MiB)
+ * per GPU, held by every GPU the library runs on until the process ends.  No
+ * call allocates (no hipMalloc, no library routine that does).  The first
+ * call on a device looks the array's address up with that device current
+ * (the caller's stream must belong to the current device; make that first
+ * call outside any stream capture).
+ * The caller still owns and passes every input and output.  Nothing in the
+ * array needs to start at zero: decode writes every partial its merge reads.
+ * Every call on one GPU shares that GPU's array and it keeps the last call's
+ * contents, so calls that overlap on one GPU (several streams, several host
+ * threads) race: serialise them.
+ * Errors: those of recache_attend_cached, and RECACHE_EWORKSPACE when
+ * recache_attend_workspace_bytes(...) for these sizes exceeds
+ * RECACHE_NOALLOC_SCRATCH_BYTES (decode with n_req * n_q_heads * splits *
+ * (head_dim + 2) fp32 partials; about 65K partial slots at head_dim 128),
+ * checked before any HIP call; RECACHE_EHIP if the address lookup fails.
+ */
+#define RECACHE_NOALLOC_SCRATCH_BYTES (32 * 1024 * 1024)
+int recache_attend_cached_noalloc(int dtype, int layer, int n_layers, int n_req,
+                                  const int32_t* cu_q, const int32_t* cu_ctx, int total_q,
+                                  int max_q, int max_ctx, int max_kv, int max_route_len,
+                                  int n_q_heads, int n_kv_heads, int head_dim, float softmax_scale,
+                                  const void* q, const void* ctx_k, const void* ctx_v,
+                                  int ctx_rows, const void* res_k, const void* res_v, int res_rows,
+                                  const int32_t* cu_kept, const int32_t* res_off,
+                                  const int32_t* route_off, const int32_t* route_res,
+                                  const int32_t* route_tokens, void* out, float* lse,
+                                  void* stream);
+
+/*
  * [host] Structural budget selection (Sec. 3, "Structural Pruning").  From
  * each layer's and each KV head group's leave-one-in contribution s_i (the
  * drop in invocation loss when only that unit sees resource states), the

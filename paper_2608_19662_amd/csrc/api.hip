@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "recache.h"
@@ -534,6 +535,81 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
     a.route_res = route_res;
     a.cu_kept = cu_kept;
     return hip_status(launch_attn_mfma(a, false, head_dim, s), "attend (prefill) launch");
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Attend without a caller workspace: decode's split partials go to a
+// library-owned static device array (for callers that cannot allocate).
+
+namespace {
+
+// One copy per GPU the library runs on, each held until the process ends.
+// In host code its name is only a stand-in: kernels get the device address
+// that hipGetSymbolAddress returns for the current device (scratch_ptr).
+static __device__ __align__(256) char scratch[RECACHE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up with
+// that device current on the first call there and kept for later calls.
+int scratch_ptr(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(RECACHE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+    REQUIRE(dev >= 0 && dev < kMaxDevices, RECACHE_EUNSUPPORTED, "device %d: at most %d devices",
+            dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(RECACHE_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return RECACHE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int recache_attend_cached_noalloc(int dtype, int layer, int n_layers, int n_req,
+                                  const int32_t* cu_q, const int32_t* cu_ctx, int total_q,
+                                  int max_q, int max_ctx, int max_kv, int max_route_len,
+                                  int n_q_heads, int n_kv_heads, int head_dim, float softmax_scale,
+                                  const void* q, const void* ctx_k, const void* ctx_v,
+                                  int ctx_rows, const void* res_k, const void* res_v, int res_rows,
+                                  const int32_t* cu_kept, const int32_t* res_off,
+                                  const int32_t* route_off, const int32_t* route_res,
+                                  const int32_t* route_tokens, void* out, float* lse,
+                                  void* stream) {
+    int rc_ = check_attend(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q, max_ctx,
+                           max_route_len, n_q_heads, n_kv_heads, head_dim, softmax_scale, q, ctx_k,
+                           ctx_v, ctx_rows, res_k, res_v, res_rows, cu_kept, res_off, route_off,
+                           route_res, route_tokens, out);
+    if (rc_) return rc_;
+    // the same workspace rule as recache_attend_cached: only bf16 decode uses one
+    const size_t need = dtype == RECACHE_BF16
+                            ? recache_attend_workspace_bytes(n_req, max_q, max_ctx, max_kv,
+                                                             n_q_heads, n_kv_heads, head_dim)
+                            : 0;
+    REQUIRE(need <= (size_t)RECACHE_NOALLOC_SCRATCH_BYTES, RECACHE_EWORKSPACE,
+            "decode needs %zu bytes of split partials, more than the %zu-byte static scratch of "
+            "the allocation-free entry point (use recache_attend_cached with a workspace)",
+            need, (size_t)RECACHE_NOALLOC_SCRATCH_BYTES);
+    void* ws = nullptr;
+    if ((rc_ = scratch_ptr(&ws))) return rc_;
+    return recache_attend_cached(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q,
+                                 max_ctx, max_kv, max_route_len, n_q_heads, n_kv_heads, head_dim,
+                                 softmax_scale, q, ctx_k, ctx_v, ctx_rows, res_k, res_v, res_rows,
+                                 cu_kept, res_off, route_off, route_res, route_tokens, out, lse, ws,
+                                 (size_t)RECACHE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int recache_check_offsets(const int32_t* cu, int n, int total, int strict) {

@@ -49,6 +49,10 @@ _SIGS = {
                                _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p, _c_p, _c_p,
                                _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                _c_p, _c_p, _c_size, _c_p], _c_int),
+    "recache_attend_cached_noalloc": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_int, _c_int,
+                                       _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p,
+                                       _c_p, _c_p, _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p,
+                                       _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_select_routes": ([_c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p,
                                _c_p, _c_p], _c_int),
     "recache_check_offsets": ([_c_p, _c_int, _c_int, _c_int], _c_int),
@@ -406,6 +410,19 @@ def attend_cached(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k
                         lse, max_kv, softmax_scale, res_off)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("recache_attend_cached", *args, _dev(workspace, "workspace"), ws_bytes, _stream(stream))
+
+
+def attend_cached_noalloc(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k, res_v,
+                          cu_kept, route_off, route_res, route_tokens, layer: int, n_layers: int,
+                          out, *, max_route_len: int, lse=None, max_kv: int = 0,
+                          softmax_scale: float = 0.0, res_off=None, stream=None):
+    """attend_cached without a workspace: decode's split partials live in the
+    library's static per-GPU scratch (see recache.h: calls that overlap on one
+    GPU race)."""
+    args = _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu_kept,
+                        route_off, route_res, route_tokens, layer, n_layers, out, max_route_len,
+                        lse, max_kv, softmax_scale, res_off)
+    _call("recache_attend_cached_noalloc", *args, _stream(stream))
 
 
 def check_offsets(cu, total: int, strict: bool = True) -> None:

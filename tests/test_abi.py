@@ -240,3 +240,21 @@ def test_python_binding_checks_shapes_first():
         rc.attend_cached(**{k: v for k, v in ga.items() if k != "max_route_len"})
     with pytest.raises(TypeError):
         rc.attend_cached(**ga)
+
+
+def test_noalloc_rejects_partials_beyond_the_scratch():
+    """The allocation-free attend checks its scratch need on the host, before
+    any HIP call: 4096 decode requests x 64 query heads need 4096 * 64 *
+    (128 + 2) * 4 bytes of split partials, more than the 32 MiB static array."""
+    L = rc.lib()
+    need = rc.attend_workspace_bytes(4096, 1, 64, 0, 64, 8, 128)
+    assert need > 32 * 1024 * 1024
+    code = L.recache_attend_cached_noalloc(1, 0, 1, 4096, FAKE, FAKE, 4096, 1, 64, 0, 4, 64, 8,
+                                           128, 0.0, FAKE, FAKE, FAKE, 64, FAKE, FAKE, 8, FAKE, None,
+                                           FAKE, FAKE, FAKE, FAKE, None, None)
+    assert code == rc.EWORKSPACE
+    assert "static scratch" in rc.last_error()
+    # and the ordinary argument checks come first
+    assert L.recache_attend_cached_noalloc(1, 5, 1, 4096, FAKE, FAKE, 4096, 1, 64, 0, 4, 64, 8,
+                                           128, 0.0, FAKE, FAKE, FAKE, 64, FAKE, FAKE, 8, FAKE,
+                                           None, FAKE, FAKE, FAKE, FAKE, None, None) == rc.EINVAL
