@@ -605,7 +605,7 @@ def headline(args, dev):
     w, flops, layers, outs, run = prefill_setup(3, dev)
     L = w.n_layers
     s = torch.cuda.current_stream()
-    t_end = time.perf_counter() + PREWARM_S
+    t_end = time.perf_counter() + args.prewarm
     while time.perf_counter() < t_end:
         run()
         torch.cuda.synchronize()
@@ -638,6 +638,8 @@ def main():
     ap.add_argument("--rows", default="all",
                     help="extra hot-path rows: all | none | comma list of row names")
     ap.add_argument("--reps", type=int, default=5, help="repetitions per extra row")
+    ap.add_argument("--prewarm", type=float, default=PREWARM_S,
+                    help="seconds of untimed load before the headline's warm-up (clock ramp)")
     ap.add_argument("--skip-headline", action="store_true",
                     help="run only the rows (for counter collection on one row)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -735,7 +737,7 @@ def main():
             "flops_per_step": h["flops"],
             "step": "36 recache_attend_cached calls (one per layer), each one launch of the "
                     "MFMA attention kernel over routed resource rows then causal context",
-            "prewarm_s": PREWARM_S,
+            "prewarm_s": args.prewarm,
         },
         "pct_of_peak": round(100.0 * h["tflops"] / PEAK_BF16_TFLOPS, 2),
         "roofline": h["roofline"],

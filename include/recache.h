@@ -49,6 +49,10 @@
  * - Element types: RECACHE_F32 (float) or RECACHE_BF16 (bfloat16); all
  *   floating tensors of one call share the dtype.  bf16 math accumulates in
  *   fp32; outputs are rounded to nearest even.  head_dim is 64 or 128.
+ * - The bf16 encode and prefill kernels address each KV plane (one KV head's
+ *   rows of a cache or of the context, a layer's route-compacted store)
+ *   through 32-bit byte offsets: a plane of 4 GiB or more (16.7M rows at
+ *   head_dim 128) is RECACHE_EUNSUPPORTED.
  * - Layouts: token-major tensors are [rows][heads][head_dim]; KV caches are
  *   head-major [kv_heads][cache_rows][head_dim], so the rows of one resource
  *   (or one request's context) for one KV group are contiguous.  GQA: query

@@ -84,6 +84,16 @@ float resolve_scale(float s, int head_dim) { return s > 0.f ? s : 1.0f / sqrtf((
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// The bf16 attention kernels read every KV plane (one KV head's rows of a
+// cache, a layer's route-compacted store, the context) through 32-bit byte
+// offsets: each must stay below 4 GiB.
+int check_planes(long rows_a, long rows_b, int head_dim) {
+    const long limit = 1L << 32, row_bytes = 2L * head_dim;
+    REQUIRE(rows_a * row_bytes < limit && rows_b * row_bytes < limit, RECACHE_EUNSUPPORTED,
+            "a KV plane of %ld or %ld rows of %ld bytes reaches 4 GiB", rows_a, rows_b, row_bytes);
+    return RECACHE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -159,17 +169,9 @@ int check_encode(int dtype, int n_res, const int32_t* cu_len, int total_T, int m
     REQUIRE(prefix_len >= 0, RECACHE_EINVAL, "prefix_len %d must be >= 0", prefix_len);
     REQUIRE(prefix_len == 0 || (prefix_k && prefix_v), RECACHE_EINVAL,
             "prefix_len %d needs prefix_k and prefix_v", prefix_len);
+    if (dtype == RECACHE_BF16)
+        if ((rc_ = check_planes(total_T, prefix_len, head_dim))) return rc_;
     return RECACHE_OK;
-}
-
-// MFMA attention tiling: a block covers 4 (query head, 32-row block) pairs of
-// one KV group, as hpw heads x rbw row blocks with hpw the largest of 4, 2, 1
-// dividing the group size (so every head of the group is covered exactly once).
-void set_tiling(AttnArgs& a, int ratio, int max_rows) {
-    a.hpw = ratio % 4 == 0 ? 4 : ratio % 2 == 0 ? 2 : 1;
-    a.rbw = 4 / a.hpw;
-    a.n_hq = ratio / a.hpw;
-    a.n_qt = (max_rows + 32 * a.rbw - 1) / (32 * a.rbw);
 }
 
 hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, int total_T,
@@ -185,7 +187,7 @@ hipError_t encode_attention_launch(int dtype, int n_res, const int32_t* cu_len, 
         a.n_q_heads = n_q_heads;
         a.n_kv_heads = n_kv_heads;
         a.ratio = ratio;
-        set_tiling(a, ratio, max_len);
+        a.max_rows = max_len;
         a.n_units = n_res;
         a.scale_log2 = scale * 1.4426950408889634f;
         a.q = static_cast<const uint16_t*>(q);
@@ -415,6 +417,8 @@ int check_attend(int dtype, int layer, int n_layers, int n_req, const int32_t* c
                 cu_kept && route_off && route_res && route_tokens && out,
             RECACHE_EINVAL, "null pointer argument");
     REQUIRE(!(isnan(softmax_scale) || isinf(softmax_scale)), RECACHE_EINVAL, "softmax_scale not finite");
+    if (dtype == RECACHE_BF16 && max_q > 1)
+        if ((rc_ = check_planes(res_rows, ctx_rows, head_dim))) return rc_;
     return RECACHE_OK;
 }
 
@@ -512,7 +516,7 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
     a.n_q_heads = n_q_heads;
     a.n_kv_heads = n_kv_heads;
     a.ratio = ratio;
-    set_tiling(a, ratio, max_q);
+    a.max_rows = max_q;
     a.n_units = n_req;
     a.scale_log2 = scale * 1.4426950408889634f;
     a.q = static_cast<const uint16_t*>(q);

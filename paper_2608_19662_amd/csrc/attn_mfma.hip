@@ -62,22 +62,27 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 constexpr int kBK = 64;  // keys per tile
-constexpr int kThreads = 256;
 constexpr int kMaxSeg = 1024;
+// Third dword of a gfx9 buffer resource for raw (unformatted) loads.
+constexpr int kBufferFlags = 0x00020000;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-template <int HD>
+template <int HD, int NW>
 struct Tile {
     static constexpr int CPR = HD / 8;           // 16-byte chunks per row
     static constexpr int ROWB = HD * 2;          // bytes per row
     static constexpr int TILEB = kBK * ROWB;     // bytes per K or V tile
     static constexpr int STAGEB = 2 * TILEB;     // K tile, then V tile
     static constexpr int RPI = 64 / CPR;         // rows per 1 KB wave copy
-    static constexpr int NJ = 16 / RPI;          // copies per wave per tile (16 rows per wave)
+    static constexpr int RPW = kBK / NW;         // rows of a tile each wave copies
+    static constexpr int NJ = RPW / RPI;         // copies per wave per tile
     static constexpr int NT = HD / 16;           // MFMA k-steps over head_dim
     static constexpr int NDB = HD / 32;          // 32-wide blocks of head_dim
+    static_assert(NJ >= 1 && RPW % RPI == 0, "each wave copies whole 1 KB runs");
+    static_assert(NW * 32 * ROWB <= 2 * STAGEB, "the output staging fits the K / V stages");
+    static_assert(NW <= 8, "at most eight waves stage their output rows");
 };
 
 // Small per-lane index sets live in vector registers rather than arrays, so
@@ -92,12 +97,15 @@ struct StageTag {
     static constexpr int value = C;
 };
 
-template <int HD, bool ENCODE>
+// The K / V tiles of the two stages are four separate LDS arrays (declared
+// in the kernel): the compiler can then tell that the copies in flight into
+// one of them do not touch the tiles being read, and issues no wait for the
+// copies before those reads.
+template <bool ENCODE, int NW>
 struct Smem {
-    alignas(16) char kv[2 * Tile<HD>::STAGEB];
     int seg_start[ENCODE ? 2 : kMaxSeg + 1];
     int seg_row[ENCODE ? 2 : kMaxSeg];
-    int scan[4];  // wave totals of the segment-length scan
+    int scan[NW];  // wave totals of the segment-length scan
 };
 
 // XOR mask of a row's chunk index: for 256-byte rows the two 2-bit halves of
@@ -112,8 +120,8 @@ __device__ __forceinline__ int chunk_mask(int row) {
 
 template <int HD>
 __device__ __forceinline__ uint32_t swz(int row, int chunk) {
-    using TL = Tile<HD>;
-    return (uint32_t)(row * TL::ROWB + ((chunk ^ chunk_mask<TL::CPR>(row)) << 4));
+    constexpr int CPR = HD / 8;
+    return (uint32_t)(row * HD * 2 + ((chunk ^ chunk_mask<CPR>(row)) << 4));
 }
 
 __device__ __forceinline__ void wait_vm0() {
@@ -126,13 +134,13 @@ __device__ __forceinline__ void wait_vm0() {
 // the outputs instead of leaving rows unwritten or dropping resources.
 // Rows [r_begin, r_end) of unit rows starting at q_row0, heads
 // [head0, head0 + n_heads).
-template <int HD>
+template <int HD, int NW>
 __device__ __forceinline__ void poison_rows(const AttnArgs& a, int head0, int n_heads, int q_row0,
                                          int r_begin, int r_end) {
     constexpr int CPR = HD / 8;
     const u32x4 nan8 = {0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};  // bf16 NaNs
     const long n = (long)max(r_end - r_begin, 0) * n_heads * CPR;
-    for (long i = threadIdx.x; i < n; i += kThreads) {
+    for (long i = threadIdx.x; i < n; i += NW * 64) {
         const int c = (int)(i % CPR);
         const long rest = i / CPR;
         const int h = head0 + (int)(rest % n_heads);
@@ -143,12 +151,16 @@ __device__ __forceinline__ void poison_rows(const AttnArgs& a, int head0, int n_
     }
 }
 
-template <int HD, bool ENCODE>
-__global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a) {
-    using TL = Tile<HD>;
+// NW waves per block, each owning one (query head, 32-row block) pair of the
+// block's KV group; two waves per SIMD either way (two 4-wave blocks or one
+// 8-wave block per CU).
+template <int HD, bool ENCODE, int NW>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnArgs a) {
+    using TL = Tile<HD, NW>;
+    constexpr int kThreads = NW * 64;
     constexpr int ROWB = TL::ROWB, TILEB = TL::TILEB, STAGEB = TL::STAGEB;
-    __shared__ Smem<HD, ENCODE> sm;
-    char* lds = sm.kv;
+    __shared__ Smem<ENCODE, NW> sm;
+    __shared__ __attribute__((aligned(16))) char k_st0[TILEB], k_st1[TILEB], v_st0[TILEB], v_st1[TILEB];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -196,7 +208,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     // the grid covers query rows [0, n_qt * wg_rows) of every unit; the block
     // of the last tile answers for any rows beyond
     if (jt == a.n_qt - 1 && q_len > a.n_qt * wg_rows) {
-        poison_rows<HD>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_len);
+        poison_rows<HD, NW>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_len);
         return;
     }
     if (q_first >= q_len) return;
@@ -209,14 +221,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         const int r0 = a.route_off[e];
         n_seg = a.route_off[e + 1] - r0;
         if (n_seg > kMaxSeg) {
-            poison_rows<HD>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_last + 1);
+            poison_rows<HD, NW>(a, g * a.ratio + hq * a.hpw, a.hpw, q_row0, q_first, q_last + 1);
             return;
         }
+        constexpr int SPT = kMaxSeg / kThreads;  // segments per thread
         int part = 0;
-        int lens[4];
+        int lens[SPT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int s = tid * 4 + i;
+        for (int i = 0; i < SPT; ++i) {
+            const int s = tid * SPT + i;
             lens[i] = 0;
             if (s < n_seg) {
                 const int r = a.route_res[r0 + s];
@@ -226,10 +239,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             }
             part += lens[i];
         }
-        int run = block4_exclusive_scan(part, sm.scan, &s_vis);
+        int run = block_exclusive_scan<NW>(part, sm.scan, &s_vis);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int s = tid * 4 + i;
+        for (int i = 0; i < SPT; ++i) {
+            const int s = tid * SPT + i;
             if (s < n_seg) sm.seg_start[s] = run;
             run += lens[i];
         }
@@ -245,29 +258,46 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     // rows outside [0, lse_rows) of q / out are never touched
     const int my_q_c = max(0, min(min(my_q, q_len - 1), (int)a.lse_rows - 1 - q_row0));
 
-    // ---- HBM -> LDS copies.  Copy j of a wave moves rows wave*16 + j*RPI +
+    // ---- HBM -> LDS copies.  Copy j of a wave moves rows wave*RPW + j*RPI +
     // [0, RPI) of a tile; lane i lands at byte 16 i of that run, i.e. row
-    // rj = wave*16 + j*RPI + i / CPR, physical chunk i % CPR, which holds
+    // rj = wave*RPW + j*RPI + i / CPR, physical chunk i % CPR, which holds
     // logical chunk (i % CPR) ^ mask(rj) of the key's row.
-    // For 256-byte rows, rj % 4 = (i / 16) % 4 and (rj / 4) % 4 = j, so the
-    // mask is ((i / 16) % 4) * 4 + j; for 128-byte rows rj % 8 = i / 8.
+    // For 256-byte rows, rj % 4 = (i / 16) % 4 and (rj / 4) % 4 = (wave*RPW/4
+    // + j) % 4, which is ((wave*RPW/4) % 4) ^ j: RPW is 16 or 8, so that term
+    // is 0 or 2 and j < NJ <= 2 adds without a carry.  For 128-byte rows
+    // rj % 8 = i / 8 whatever the wave and j (RPW and RPI are multiples of 8).
+    static_assert(TL::CPR != 16 || (TL::RPW % 8 == 0 && TL::NJ <= 2) || TL::RPW % 16 == 0,
+                  "copy j's chunk mask is copy 0's xor j");
     const int cp_lane_row = lane / TL::CPR;
-    const int cp_chunk0 = (lane % TL::CPR) ^ chunk_mask<TL::CPR>(wave * 16 + cp_lane_row);
+    const int cp_chunk0 = (lane % TL::CPR) ^ chunk_mask<TL::CPR>(wave * TL::RPW + cp_lane_row);
     auto cp_chunk = [&](int j) { return TL::CPR == 16 ? (cp_chunk0 ^ j) : cp_chunk0; };
-    // Where one tile comes from.  A "fast" tile lies inside one segment (the
-    // prefix, in encode) or inside the context (the resource's own rows, in
-    // encode): its 64 rows are consecutive, so each copy reads a wave-uniform
-    // base plus a per-lane constant, with no per-lane address arithmetic.
-    // Tiles that straddle a boundary or the end of the stream take per-lane
-    // addresses: K addresses plus a flag per key for the buffer it is in.
-    u32v<TL::NJ> lane_off;  // this lane's element offset within a run of 64 rows
+    // Where one tile comes from.  Every copy is a buffer load into LDS from
+    // one of four planes, each a buffer resource built once per block: the
+    // group's segment rows (K and V) and its causal rows (K and V).  Buffer
+    // loads are bounds-checked (reads past a plane return zeros) and leave the
+    // compiler's LDS wait counting exact, which the flat-address form of the
+    // LDS copy does not.  A "fast" tile lies inside one segment (the prefix,
+    // in encode) or inside the causal rows: its 64 rows are consecutive, so
+    // each copy takes the tile's byte offset in a scalar register plus a
+    // per-lane constant, with no per-lane address arithmetic.  Tiles that
+    // straddle a boundary or the end of the stream take per-lane offsets and
+    // a flag per key for the plane it is in (one exec-masked load per plane).
+    const __amdgpu_buffer_rsrc_t rs_k = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.k + (size_t)g * a.k_gstride * HD), (short)0, (int)(a.k_rows * ROWB), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rs_v = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.v + (size_t)g * a.k_gstride * HD), (short)0, (int)(a.k_rows * ROWB), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rc_k = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.ck + (size_t)g * a.c_rows * HD), (short)0, (int)(a.c_rows * ROWB), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rc_v = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.cv + (size_t)g * a.c_rows * HD), (short)0, (int)(a.c_rows * ROWB), kBufferFlags);
+    u32v<TL::NJ> lane_off;  // this lane's byte offset within a run of 64 rows
 #pragma unroll
     for (int j = 0; j < TL::NJ; ++j)
-        lane_off[j] = (uint32_t)(wave * 16 + j * TL::RPI + cp_lane_row) * HD + cp_chunk(j) * 8;
-    bool t_fast = false;  // wave-uniform
-    const uint16_t* t_kb = a.k;
-    const uint16_t* t_vb = a.v;
-    u64v<TL::NJ> kp = {};
+        lane_off[j] = ((uint32_t)(wave * TL::RPW + j * TL::RPI + cp_lane_row) * HD + cp_chunk(j) * 8) * 2;
+    bool t_fast = false;   // wave-uniform
+    bool t_ctx = false;    // wave-uniform: a fast tile of the causal rows
+    uint32_t t_off = 0;    // wave-uniform: byte offset of a fast tile's first row in its plane
+    u32v<TL::NJ> voff = {};
     uint32_t in_ctx = 0;
     // Streams visit segments in order.  The wave keeps the segment of its
     // current tile's first key (for the fast test), and each lane the segment
@@ -286,75 +316,71 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     }
     auto key_ptrs = [&](int kt) {
         const int p0 = kt * kBK;
-        {
-            t_fast = false;
-            if (p0 + kBK <= s_vis) {
-                while (p0 >= u_hi && u_sidx + 1 < n_seg) {
-                    ++u_sidx;
-                    u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx + 1]);
-                    u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[u_sidx]) -
-                           __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx]);
-                }
-                const long row0 = (long)u_dl + p0;
-                if (p0 + kBK <= u_hi && row0 >= 0 && row0 + kBK <= a.k_rows) {
-                    t_fast = true;
-                    t_kb = a.k + ((size_t)g * a.k_gstride + row0) * HD;
-                    t_vb = a.v + ((size_t)g * a.k_gstride + row0) * HD;
-                }
-            } else if (p0 >= s_vis && p0 + kBK <= stream) {
-                const long row0 = (long)ctx_row0 + (p0 - s_vis);
-                if (row0 + kBK <= a.c_rows) {
-                    t_fast = true;
-                    t_kb = a.ck + ((size_t)g * a.c_rows + row0) * HD;
-                    t_vb = a.cv + ((size_t)g * a.c_rows + row0) * HD;
-                }
+        t_fast = false;
+        if (p0 + kBK <= s_vis) {
+            while (p0 >= u_hi && u_sidx + 1 < n_seg) {
+                ++u_sidx;
+                u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx + 1]);
+                u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[u_sidx]) -
+                       __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx]);
             }
-            if (!t_fast) {
-                static_for<TL::NJ>([&](auto jc) {
-                    constexpr int j = decltype(jc)::value;
-                    const int p = min(p0 + wave * 16 + j * TL::RPI + cp_lane_row, stream - 1);
-                    if (p < s_vis) {
-                        while (p >= seg_hi && sidx + 1 < n_seg) {
-                            ++sidx;
-                            seg_hi = sm.seg_start[sidx + 1];
-                            seg_dl = sm.seg_row[sidx] - sm.seg_start[sidx];
-                        }
-                        const size_t row = min((size_t)(seg_dl + p), (size_t)a.k_rows - 1);
-                        kp[j] = (uint64_t)(a.k + ((size_t)g * a.k_gstride + row) * HD + cp_chunk(j) * 8);
-                        in_ctx &= ~(1u << j);
-                    } else {
-                        const size_t row = min((size_t)ctx_row0 + (p - s_vis), (size_t)a.c_rows - 1);
-                        kp[j] = (uint64_t)(a.ck + ((size_t)g * a.c_rows + row) * HD + cp_chunk(j) * 8);
-                        in_ctx |= 1u << j;
+            const long row0 = (long)u_dl + p0;
+            if (p0 + kBK <= u_hi && row0 >= 0 && row0 + kBK <= a.k_rows) {
+                t_fast = true;
+                t_ctx = false;
+                t_off = (uint32_t)row0 * ROWB;
+            }
+        } else if (p0 >= s_vis && p0 + kBK <= stream) {
+            const long row0 = (long)ctx_row0 + (p0 - s_vis);
+            if (row0 + kBK <= a.c_rows) {
+                t_fast = true;
+                t_ctx = true;
+                t_off = (uint32_t)row0 * ROWB;
+            }
+        }
+        if (!t_fast) {
+            static_for<TL::NJ>([&](auto jc) {
+                constexpr int j = decltype(jc)::value;
+                const int p = min(p0 + wave * TL::RPW + j * TL::RPI + cp_lane_row, stream - 1);
+                uint32_t row;
+                if (p < s_vis) {
+                    while (p >= seg_hi && sidx + 1 < n_seg) {
+                        ++sidx;
+                        seg_hi = sm.seg_start[sidx + 1];
+                        seg_dl = sm.seg_row[sidx] - sm.seg_start[sidx];
                     }
-                });
-            }
+                    row = (uint32_t)(seg_dl + p);
+                    in_ctx &= ~(1u << j);
+                } else {
+                    row = (uint32_t)(ctx_row0 + (p - s_vis));
+                    in_ctx |= 1u << j;
+                }
+                voff[j] = row * ROWB + cp_chunk(j) * 16;
+            });
         }
     };
-    // the same element of V: the two buffers share their layout
-    const ptrdiff_t v_res = a.v - a.k, v_ctx = a.cv - a.ck;
-    auto copy = [&](bool is_v, int dst_byte) {
-        char* dst = lds + dst_byte + wave * 16 * ROWB;
-        // Per-copy addresses first, then one sequence of copies: the two
-        // paths only differ in how the addresses are formed.
-        u64v<TL::NJ> src;
+    // (the offsets are passed as int, the builtin's parameter type: handed an
+    // unsigned vector element, the host pass drops the kernel's launch stub)
+    auto copy = [&](bool is_v, char* buf) {
+        char* dst = buf + wave * TL::RPW * ROWB;
         if (t_fast) {
-            const uint16_t* base = is_v ? t_vb : t_kb;
-            static_for<TL::NJ>([&](auto jc) {
-                constexpr int j = decltype(jc)::value;
-                src[j] = (uint64_t)(base + lane_off[j]);
-            });
+            const __amdgpu_buffer_rsrc_t r = t_ctx ? (is_v ? rc_v : rc_k) : (is_v ? rs_v : rs_k);
+#pragma unroll
+            for (int j = 0; j < TL::NJ; ++j)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
+                                                         (int)lane_off[j], (int)t_off, 0, 0);
         } else {
-            static_for<TL::NJ>([&](auto jc) {
-                constexpr int j = decltype(jc)::value;
-                src[j] = is_v ? kp[j] + 2 * ((in_ctx >> j) & 1 ? v_ctx : v_res) : kp[j];
-            });
+            const __amdgpu_buffer_rsrc_t rs = is_v ? rs_v : rs_k, rc = is_v ? rc_v : rc_k;
+#pragma unroll
+            for (int j = 0; j < TL::NJ; ++j) {
+                if ((in_ctx >> j) & 1)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
+                                                             (int)voff[j], 0, 0, 0);
+                else
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
+                                                             (int)voff[j], 0, 0, 0);
+            }
         }
-        static_for<TL::NJ>([&](auto jc) {
-            constexpr int j = decltype(jc)::value;
-            __builtin_amdgcn_global_load_lds((const void*)src[j], (lds_void*)(dst + j * TL::RPI * ROWB), 16,
-                                             0, 0);
-        });
     };
 
     // Query rows first (they are needed first, for the RoPE), then the
@@ -368,11 +394,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             qraw[t] = *reinterpret_cast<const u32x4*>(qrow + t * 16 + half * 8);
     }
     key_ptrs(0);
-    copy(false, 0);
-    copy(true, TILEB);
+    copy(false, k_st0);
+    copy(true, v_st0);
     if (n_tiles > 1) {
         key_ptrs(1);
-        copy(false, STAGEB);
+        copy(false, k_st1);
     }
 
     // ---- Q fragment (B operand of S^T = K Q^T): lane holds row my_q, elements
@@ -389,11 +415,11 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             // row, so the 16 rows read by a lane group fall on distinct banks.
             // Larger blocks compute their lane's 32 frequencies directly.
             constexpr int HALF = HD / 2;
-            const char* tab = lds + STAGEB + TILEB;
+            const char* tab = v_st1;
             const bool use_tab = wg_rows <= 32;
             const int r = my_q - q_first;
             if (use_tab) {
-                char* wtab = lds + STAGEB + TILEB;
+                char* wtab = v_st1;
                 for (int idx = tid; idx < wg_rows * HALF; idx += kThreads) {
                     const int rr = idx / HALF, f = idx % HALF;
                     float sn, cs;
@@ -460,7 +486,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         const int G = lane >> 4, i = lane & 15;
         const int row = (G >> 1) * 4 + (i >> 2);
         const int col = (G & 1) * 16 + (i & 3) * 4;
-        v_rd0 = TILEB + swz<HD>(row, col >> 3) + (col & 7) * 2;
+        v_rd0 = swz<HD>(row, col >> 3) + (col & 7) * 2;
     }
     auto v_rd = [&](int db, int w) -> uint32_t {
         return v_rd0 ^ (uint32_t)(db << 6) ^ (uint32_t)(w * (8 * ROWB + (TL::CPR == 16 ? 32 : 0)));
@@ -480,7 +506,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
 
     wait_vm0();
     __syncthreads();  // K(0), V(0), K(1) in LDS; RoPE table reads done
-    qk(sacc[0], lds);
+    qk(sacc[0], k_st0);
     __syncthreads();  // every wave has read K(0) before K(2) is copied over it
 
     const float sl2 = a.scale_log2;
@@ -500,10 +526,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
     auto tile = [&](auto stage_tag, auto next_tag, int kt) {
         constexpr int cur = decltype(stage_tag)::value;
         constexpr bool NEXT = decltype(next_tag)::value != 0;
-        if constexpr (NEXT) copy(true, (cur ^ 1) * STAGEB + TILEB);
+        if constexpr (NEXT) copy(true, cur ? v_st0 : v_st1);
         if (kt + 2 < n_tiles) {
             key_ptrs(kt + 2);
-            copy(false, cur * STAGEB);
+            copy(false, cur ? k_st1 : k_st0);
         }
         f32x16* sc = sacc[cur];
         // causal / stream-end mask, only on tiles that reach past the first row's limit
@@ -534,7 +560,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             m = m_new;
         }
         // S(t + 1) on the matrix pipe while the weights of tile t are formed.
-        if constexpr (NEXT) qk(sacc[cur ^ 1], lds + (cur ^ 1) * STAGEB);
+        if constexpr (NEXT) qk(sacc[cur ^ 1], cur ? k_st0 : k_st1);
         const float msl = m * sl2;
         bf16x8 pf[4];
 #pragma unroll
@@ -566,7 +592,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        const char* st = lds + cur * STAGEB;
+        const char* st = cur ? v_st1 : v_st0;
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db) {
 #pragma unroll
@@ -618,7 +644,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
         const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
         const int row = ln & 31, hf = ln >> 5;  // this lane's row, and which half of it
         constexpr int CPR = TL::CPR;
-        char* ob = lds + wave * 32 * ROWB;
+        // two waves' 32 rows per K / V tile array
+        static_assert(TILEB == 2 * 32 * ROWB, "two waves stage their rows in one tile array");
+        const int wb = wave >> 1;
+        char* ob = (wb == 0 ? k_st0 : wb == 1 ? v_st0 : wb == 2 ? k_st1 : v_st1) + (wave & 1) * 32 * ROWB;
         const float inv = 1.0f / l;
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db)
@@ -649,22 +678,50 @@ __global__ __launch_bounds__(kThreads, 2) void attn_mfma_kernel(const AttnArgs a
 
 }  // namespace
 
-hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream) {
-    const long blocks = (long)a.n_qt * a.n_units * a.n_hq * a.n_kv_heads;
+namespace {
+
+// Waves per block of each mode: encode's blocks are short (a few tiles per
+// resource), so two 4-wave blocks per CU overlap one block's prologue with
+// the other's loop; prefill streams long key lists, where one 8-wave block
+// per CU copies each K / V tile once for twice the query rows.
+constexpr int kEncodeWaves = 4;
+constexpr int kAttendWaves = 8;
+
+// A block covers NW (query head, 32-row block) pairs of one KV group: hpw
+// heads x rbw row blocks, hpw the largest power of two up to NW dividing the
+// group size, so every head of the group is covered exactly once.
+template <int NW>
+void set_tiling(AttnArgs& b) {
+    int h = NW;
+    while (b.ratio % h) h >>= 1;
+    b.hpw = h;
+    b.rbw = NW / h;
+    b.n_hq = b.ratio / h;
+    b.n_qt = (b.max_rows + 32 * b.rbw - 1) / (32 * b.rbw);
+}
+
+template <int HD, bool ENCODE, int NW>
+hipError_t launch(const AttnArgs& a, hipStream_t stream) {
+    AttnArgs b = a;
+    set_tiling<NW>(b);
+    b.lazy = 8.0f / a.scale_log2;
+    const long blocks = (long)b.n_qt * b.n_units * b.n_hq * b.n_kv_heads;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
-    if (a.hpw * a.rbw != 4) return hipErrorInvalidValue;  // one (head, row block) pair per wave
-    dim3 grid((unsigned)blocks), block(kThreads);
-    AttnArgs b = a;
-    b.lazy = 8.0f / a.scale_log2;
-    if (head_dim == 128) {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<128, true>), grid, block, 0, stream, b);
-        else hipLaunchKernelGGL((attn_mfma_kernel<128, false>), grid, block, 0, stream, b);
-    } else {
-        if (encode) hipLaunchKernelGGL((attn_mfma_kernel<64, true>), grid, block, 0, stream, b);
-        else hipLaunchKernelGGL((attn_mfma_kernel<64, false>), grid, block, 0, stream, b);
-    }
+    hipLaunchKernelGGL((attn_mfma_kernel<HD, ENCODE, NW>), dim3((unsigned)blocks), dim3(NW * 64), 0,
+                       stream, b);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream) {
+    if (a.ratio < 1 || a.max_rows < 1) return hipErrorInvalidValue;
+    if (head_dim == 128)
+        return encode ? launch<128, true, kEncodeWaves>(a, stream)
+                      : launch<128, false, kAttendWaves>(a, stream);
+    return encode ? launch<64, true, kEncodeWaves>(a, stream)
+                  : launch<64, false, kAttendWaves>(a, stream);
 }
 
 }  // namespace rc

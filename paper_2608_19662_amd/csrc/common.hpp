@@ -87,11 +87,12 @@ __device__ __forceinline__ float wave_sum(float x) {
     return x;
 }
 
-// Exclusive prefix sum of `part` over the threads of a 4-wave block, in
+// Exclusive prefix sum of `part` over the threads of an NW-wave block, in
 // thread order, and the block total: lane shuffles inside each wave, then
-// the four wave totals through `wave_tot` (LDS, 4 ints).  One barrier; every
+// the NW wave totals through `wave_tot` (LDS, NW ints).  One barrier; every
 // thread of the block must call it.
-__device__ __forceinline__ int block4_exclusive_scan(int part, int* wave_tot, int* total) {
+template <int NW>
+__device__ __forceinline__ int block_exclusive_scan(int part, int* wave_tot, int* total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int incl = part;
     for (int o = 1; o < 64; o <<= 1) {
@@ -100,10 +101,19 @@ __device__ __forceinline__ int block4_exclusive_scan(int part, int* wave_tot, in
     }
     if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
-    int before = 0;
-    for (int w = 0; w < wave; ++w) before += wave_tot[w];
-    *total = wave_tot[0] + wave_tot[1] + wave_tot[2] + wave_tot[3];
+    int before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const int t = wave_tot[w];
+        if (w < wave) before += t;
+        tot += t;
+    }
+    *total = tot;
     return before + incl - part;
+}
+
+__device__ __forceinline__ int block4_exclusive_scan(int part, int* wave_tot, int* total) {
+    return block_exclusive_scan<4>(part, wave_tot, total);
 }
 
 }  // namespace rc

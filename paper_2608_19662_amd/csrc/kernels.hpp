@@ -12,13 +12,14 @@ namespace rc {
 
 // bf16 MFMA flash attention (encode or conversation prefill).
 struct AttnArgs {
-    // decomposition: blocks = n_qt * n_units * n_hq * n_kv_heads
+    // decomposition: blocks = n_qt * n_units * n_hq * n_kv_heads; the
+    // launcher fills hpw, rbw, n_hq and n_qt from ratio and max_rows
     int n_q_heads, n_kv_heads, ratio;
-    int hpw;      // query heads per block (largest of 4, 2, 1 dividing ratio)
-    int rbw;      // 32-row blocks per block (4 / hpw: one (head, row block) pair per wave)
+    int hpw;      // query heads per block (largest power of two <= waves dividing ratio)
+    int rbw;      // 32-row blocks per block (waves / hpw: one (head, row block) pair per wave)
     int n_hq;     // blocks per group along heads (ratio / hpw)
     int n_units;  // resources (encode) or requests (prefill)
-    int n_qt;     // query tiles per unit (ceil(max rows / (32 * rbw)))
+    int n_qt;     // query tiles per unit (ceil(max_rows / (32 * rbw)))
     float scale_log2;  // softmax_scale * log2(e)
     float lazy;        // rescale threshold 8 / scale_log2 (set by the launch)
     const uint16_t* q;
@@ -48,6 +49,7 @@ struct AttnArgs {
     const int32_t* route_res;
     const int32_t* cu_kept;
     const int32_t* res_off;  // route-compacted store rows [n_res * Hkv], or NULL
+    int max_rows;            // query rows of the longest unit (the grid covers no more)
 };
 hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream);
 
