@@ -272,36 +272,50 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
     const int cp_chunk0 = (lane % TL::CPR) ^ chunk_mask<TL::CPR>(wave * TL::RPW + cp_lane_row);
     auto cp_chunk = [&](int j) { return TL::CPR == 16 ? (cp_chunk0 ^ j) : cp_chunk0; };
     // Where one tile comes from.  Every copy is a buffer load into LDS from
-    // one of four planes, each a buffer resource built once per block: the
-    // group's segment rows (K and V) and its causal rows (K and V).  Buffer
-    // loads are bounds-checked (reads past a plane return zeros) and leave the
+    // one of four planes: the group's segment rows (K and V; the shared
+    // prefix in encode) and its causal rows (K and V; the resource's own rows
+    // in encode), each addressed through a buffer resource.  Buffer loads are
+    // bounds-checked (reads past a plane return zeros) and leave the
     // compiler's LDS wait counting exact, which the flat-address form of the
-    // LDS copy does not.  A "fast" tile lies inside one segment (the prefix,
-    // in encode) or inside the causal rows: its 64 rows are consecutive, so
-    // each copy takes the tile's byte offset in a scalar register plus a
-    // per-lane constant, with no per-lane address arithmetic.  Tiles that
-    // straddle a boundary or the end of the stream take per-lane offsets and
+    // LDS copy does not.
+    //
+    // The stream is walked as "runs" of stream positions whose rows are
+    // consecutive in one plane (one segment, or the whole causal part).  The
+    // wave keeps the current run's end, the byte offset of stream position 0
+    // in the run's plane (modulo 2^32) and the run's two resources, so a tile
+    // inside the run costs a compare and an add: each copy takes the tile's
+    // offset in a scalar register plus a per-lane constant.  Only a tile that
+    // crosses the end of a run, or of the stream, takes per-lane offsets and
     // a flag per key for the plane it is in (one exec-masked load per plane).
-    const __amdgpu_buffer_rsrc_t rs_k = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.k + (size_t)g * a.k_gstride * HD), (short)0, (int)(a.k_rows * ROWB), kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rs_v = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.v + (size_t)g * a.k_gstride * HD), (short)0, (int)(a.k_rows * ROWB), kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rc_k = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.ck + (size_t)g * a.c_rows * HD), (short)0, (int)(a.c_rows * ROWB), kBufferFlags);
-    const __amdgpu_buffer_rsrc_t rc_v = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.cv + (size_t)g * a.c_rows * HD), (short)0, (int)(a.c_rows * ROWB), kBufferFlags);
+    auto plane_k = [&](bool causal) {
+        return causal ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.ck + (size_t)g * a.c_rows * HD), (short)0,
+                                                          (int)(a.c_rows * ROWB), kBufferFlags)
+                      : __builtin_amdgcn_make_buffer_rsrc((void*)(a.k + (size_t)g * a.k_gstride * HD), (short)0,
+                                                          (int)(a.k_rows * ROWB), kBufferFlags);
+    };
+    auto plane_v = [&](bool causal) {
+        return causal ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.cv + (size_t)g * a.c_rows * HD), (short)0,
+                                                          (int)(a.c_rows * ROWB), kBufferFlags)
+                      : __builtin_amdgcn_make_buffer_rsrc((void*)(a.v + (size_t)g * a.k_gstride * HD), (short)0,
+                                                          (int)(a.k_rows * ROWB), kBufferFlags);
+    };
     u32v<TL::NJ> lane_off;  // this lane's byte offset within a run of 64 rows
 #pragma unroll
     for (int j = 0; j < TL::NJ; ++j)
         lane_off[j] = ((uint32_t)(wave * TL::RPW + j * TL::RPI + cp_lane_row) * HD + cp_chunk(j) * 8) * 2;
-    bool t_fast = false;   // wave-uniform
-    bool t_ctx = false;    // wave-uniform: a fast tile of the causal rows
-    uint32_t t_off = 0;    // wave-uniform: byte offset of a fast tile's first row in its plane
+    // the current run (wave-uniform)
+    int run_hi = 0;           // first stream position past the run (0: no run yet)
+    bool run_causal = true;   // the run's plane: causal rows, or segment rows
+    uint32_t run_off0 = 0;    // byte offset of stream position 0 in the run's plane, mod 2^32
+    __amdgpu_buffer_rsrc_t run_k = plane_k(true), run_v = plane_v(true);
+    // the tile being set up (wave-uniform, except the per-lane straddle data)
+    bool t_fast = false;
+    uint32_t t_off = 0;
     u32v<TL::NJ> voff = {};
     uint32_t in_ctx = 0;
-    // Streams visit segments in order.  The wave keeps the segment of its
-    // current tile's first key (for the fast test), and each lane the segment
-    // of its current key (for straddling tiles); both only move forward.
+    // Streams visit segments in order.  The wave keeps the segment of the
+    // current run (u_*), each lane the segment of its current key for
+    // straddling tiles (sidx, ...); both only move forward.
     int u_sidx = 0, u_hi = 0, u_dl = 0;
     int sidx = 0, seg_hi = 0, seg_dl = 0;
     if (n_seg > 0) {
@@ -316,28 +330,34 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
     }
     auto key_ptrs = [&](int kt) {
         const int p0 = kt * kBK;
-        t_fast = false;
-        if (p0 + kBK <= s_vis) {
-            while (p0 >= u_hi && u_sidx + 1 < n_seg) {
-                ++u_sidx;
-                u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx + 1]);
-                u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[u_sidx]) -
-                       __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx]);
-            }
-            const long row0 = (long)u_dl + p0;
-            if (p0 + kBK <= u_hi && row0 >= 0 && row0 + kBK <= a.k_rows) {
-                t_fast = true;
-                t_ctx = false;
-                t_off = (uint32_t)row0 * ROWB;
-            }
-        } else if (p0 >= s_vis && p0 + kBK <= stream) {
-            const long row0 = (long)ctx_row0 + (p0 - s_vis);
-            if (row0 + kBK <= a.c_rows) {
-                t_fast = true;
-                t_ctx = true;
-                t_off = (uint32_t)row0 * ROWB;
+        if (p0 + kBK > run_hi) {
+            // leave the current run: find the one containing p0
+            if (p0 < s_vis) {
+                while (p0 >= u_hi && u_sidx + 1 < n_seg) {
+                    ++u_sidx;
+                    u_hi = __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx + 1]);
+                    u_dl = __builtin_amdgcn_readfirstlane(sm.seg_row[u_sidx]) -
+                           __builtin_amdgcn_readfirstlane(sm.seg_start[u_sidx]);
+                }
+                if (run_causal) {  // entering the segment plane
+                    run_causal = false;
+                    run_k = plane_k(false);
+                    run_v = plane_v(false);
+                }
+                run_hi = u_hi;
+                run_off0 = (uint32_t)u_dl * ROWB;
+            } else {
+                run_hi = stream;  // (run_k / run_v start on the causal plane)
+                if (!run_causal) {  // entering the causal plane
+                    run_causal = true;
+                    run_k = plane_k(true);
+                    run_v = plane_v(true);
+                }
+                run_off0 = (uint32_t)(ctx_row0 - s_vis) * ROWB;
             }
         }
+        t_fast = p0 + kBK <= run_hi;
+        t_off = run_off0 + (uint32_t)p0 * ROWB;
         if (!t_fast) {
             static_for<TL::NJ>([&](auto jc) {
                 constexpr int j = decltype(jc)::value;
@@ -364,21 +384,32 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
     auto copy = [&](bool is_v, char* buf) {
         char* dst = buf + wave * TL::RPW * ROWB;
         if (t_fast) {
-            const __amdgpu_buffer_rsrc_t r = t_ctx ? (is_v ? rc_v : rc_k) : (is_v ? rs_v : rs_k);
+            const __amdgpu_buffer_rsrc_t r = is_v ? run_v : run_k;
 #pragma unroll
             for (int j = 0; j < TL::NJ; ++j)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
                                                          (int)lane_off[j], (int)t_off, 0, 0);
         } else {
-            const __amdgpu_buffer_rsrc_t rs = is_v ? rs_v : rs_k, rc = is_v ? rc_v : rc_k;
+            const __amdgpu_buffer_rsrc_t rs = is_v ? plane_v(false) : plane_k(false);
+            const __amdgpu_buffer_rsrc_t rc = is_v ? plane_v(true) : plane_k(true);
 #pragma unroll
             for (int j = 0; j < TL::NJ; ++j) {
-                if ((in_ctx >> j) & 1)
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
-                                                             (int)voff[j], 0, 0, 0);
-                else
-                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + j * TL::RPI * ROWB), 16,
-                                                             (int)voff[j], 0, 0, 0);
+                // The rows of one copy lie in one plane except where the
+                // segments end and the causal rows begin (once per stream):
+                // choose the resource on a wave-uniform test, and only that
+                // rare mixed copy picks it per lane.
+                const bool c = (in_ctx >> j) & 1;
+                const uint64_t m = __builtin_amdgcn_ballot_w64(c);
+                lds_void* d = (lds_void*)(dst + j * TL::RPI * ROWB);
+                if (m == 0) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, (int)voff[j], 0, 0, 0);
+                } else if (m == __builtin_amdgcn_read_exec()) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, d, 16, (int)voff[j], 0, 0, 0);
+                } else if (c) {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, d, 16, (int)voff[j], 0, 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, (int)voff[j], 0, 0, 0);
+                }
             }
         }
     };
