@@ -204,6 +204,11 @@ def prefill_setup(k, dev):
     w = config(k)["attend"]
     L, r = w.n_layers, w.n_q_heads // w.n_kv_heads
     flops = 4.0 * w.head_dim * r * float(prefill_pairs(w).sum())
+    # algorithmic bytes of one launch (mean over layers): Q in, O out, and K
+    # and V of every route-visible kept row and every context row once per
+    # (request, KV group)
+    kv_rows = float(visible_tokens(w).sum()) / L + float(w.cu_ctx[-1]) * w.n_kv_heads
+    nbytes = (2.0 * float(w.cu_q[-1]) * w.n_q_heads + 2.0 * kv_rows) * w.head_dim * 2
     layers = [w.layer_tensors(l, dev) for l in range(L)]
     outs = [torch.empty_like(t[0]) for t in layers]
     st = _routes(w, dev)
@@ -214,21 +219,22 @@ def prefill_setup(k, dev):
             rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], int(w.q_lens.max()),
                              int(w.ctx_lens.max()), rk, rv, st["cu_rows"], st["route_off"],
                              st["route_res"], st["route_tokens"], l, L, outs[l],
-                             max_route_len=st["max_route_len"])
+                             max_route_len=st["max_route_len"], plan=st["plan"])
 
-    return w, flops, layers, outs, run
+    return w, flops, nbytes, layers, outs, run
 
 
 def prefill_row(k, dev, reps):
     import torch
 
-    w, flops, layers, outs, run = prefill_setup(k, dev)
+    w, flops, nbytes, layers, outs, run = prefill_setup(k, dev)
     L = w.n_layers
     ms = timed(run, reps)
     res = {"workload": "config %d" % k, "layers": L, "ms_per_pass": ms,
            "tflops": flops / (ms * 1e-3) / 1e12, "flops": flops,
            "roofline": roofline("attn_mfma_kernel<128, attend>", "mfma", flops / L, ms / L,
-                                traffic=measured_traffic(PREFILL_TRAFFIC[k]), launches=reps * L)}
+                                traffic=measured_traffic(PREFILL_TRAFFIC[k]), launches=reps * L,
+                                algorithmic_bytes=nbytes)}
     res["pct_of_peak"] = 100.0 * res["tflops"] / PEAK_BF16_TFLOPS
     del layers, outs
     torch.cuda.empty_cache()
@@ -250,6 +256,12 @@ def _routes(w, dev):
                   torch.from_numpy(w.mask).to(dev), st["cu_rows"], st["route_off"],
                   st["route_res"], st["route_tokens"])
     rc.build_routes(*st["args"])
+    st["plan"] = None
+    if USE_PLAN:
+        st["plan"] = torch.empty(w.n_layers, w.n_req * w.n_kv_heads, dtype=torch.int32, device=dev)
+        st["plan_args"] = (st["cu_q"], st["cu_ctx"], st["route_tokens"], w.n_layers, w.n_q_heads,
+                           w.n_kv_heads, st["plan"])
+        rc.attend_plan(*st["plan_args"])
     return st
 
 
@@ -279,11 +291,12 @@ def decode_row(dev, reps):
             rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], 1, int(w.ctx_lens.max()), rk, rv,
                              st["cu_rows"], st["route_off"], st["route_res"], st["route_tokens"], l,
                              L, outs[l], workspace=ws, max_kv=max_kv,
-                             max_route_len=st["max_route_len"])
+                             max_route_len=st["max_route_len"], plan=st["plan"])
 
     ms = timed(run, reps)
     gbs = (kv_bytes + qo_bytes) / (ms * 1e-3) / 1e9
     route_ms = timed(lambda: rc.build_routes(*st["args"]), reps)
+    plan_ms = timed(lambda: rc.attend_plan(*st["plan_args"]), reps) if USE_PLAN else None
     res = {"workload": "config 5", "layers": L, "ms_per_step": ms, "gbs": gbs,
            "pct_of_peak": 100.0 * gbs / PEAK_HBM_GBS, "bytes": kv_bytes + qo_bytes,
            "resident_gb": sum(t.numel() * t.element_size() for lt in layers for t in lt) / 1e9,
@@ -295,7 +308,7 @@ def decode_row(dev, reps):
     del layers, outs
     torch.cuda.empty_cache()
     return res, {"workload": "config 5 (64 req x 36 layers x 8 groups)", "ms": route_ms,
-                 "entries": int(w.n_req * L * G)}
+                 "entries": int(w.n_req * L * G), "plan_ms_36_layers": plan_ms}
 
 
 def route_store_row(dev, reps):
@@ -350,7 +363,7 @@ def route_store_row(dev, reps):
             rc.attend_cached(q, ck, cv, st["cu_q"], st["cu_ctx"], 1, int(w.ctx_lens.max()), ks[l],
                              vs[l], st["cu_rows"], st["route_off"], st["route_res"],
                              st["route_tokens"], l, L, outs[l], workspace=ws, max_kv=max_kv,
-                             max_route_len=st["max_route_len"], res_off=off[l])
+                             max_route_len=st["max_route_len"], res_off=off[l], plan=st["plan"])
 
     ms = timed(run, reps)
     gbs = io_bytes / (ms * 1e-3) / 1e9
@@ -403,6 +416,10 @@ def prune_row(dev, reps):
             "pct_of_peak": 100.0 * nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, "rows_kept": K,
             "launches": reps, "note": "back-to-back launches queued behind a fill"}
 
+
+# attend with the per-batch work order (recache_attend_plan), built with the
+# routes, outside the timed steps like them
+USE_PLAN = True
 
 PROFILES = os.path.join(ROOT, "profiles")
 ENCODE_TRAFFIC = ("attn_mfma_encode_config2_traffic.md", ("attn_mfma.hip", "common.hpp", "kernels.hpp"))
@@ -528,6 +545,11 @@ def dense_decode_row(dev, reps):
     mask = torch.ones(w.n_res, L, G, dtype=torch.uint8, device=dev)
     rc.build_routes(i32(w.req_res_off, dev), i32(w.req_res, dev), mask, cu_rows, route_off,
                     route_res, route_tokens)
+    cu_q, cu_ctx = i32(w.cu_q, dev), i32(w.cu_ctx, dev)
+    plan = None
+    if USE_PLAN:
+        plan = torch.empty(L, w.n_req * G, dtype=torch.int32, device=dev)
+        rc.attend_plan(cu_q, cu_ctx, route_tokens, L, Hq, G, plan)
     per_req = np.array([int(w.lengths[w.req_res[w.req_res_off[b]:w.req_res_off[b + 1]]].sum())
                         for b in range(w.n_req)], np.int64)
     keys = per_req + w.ctx_lens.astype(np.int64)
@@ -535,14 +557,13 @@ def dense_decode_row(dev, reps):
     nb = rc.attend_workspace_bytes(w.n_req, 1, int(w.ctx_lens.max()), max_kv, Hq, G, d)
     ws = torch.empty(nb // 4, dtype=torch.float32, device=dev)
     out = torch.empty_like(q)
-    cu_q, cu_ctx = i32(w.cu_q, dev), i32(w.cu_ctx, dev)
     max_route = int(np.diff(w.req_res_off).max())
 
     def run():
         for l in range(L):
             rc.attend_cached(q, ck, cv, cu_q, cu_ctx, 1, int(w.ctx_lens.max()), rk, rv, cu_rows,
                              route_off, route_res, route_tokens, l, L, out, workspace=ws,
-                             max_kv=max_kv, max_route_len=max_route)
+                             max_kv=max_kv, max_route_len=max_route, plan=plan)
 
     ms = timed(run, reps)
     nbytes = (float(keys.sum()) * G * 4 * d + 2.0 * w.n_req * Hq * d * 2) * L
@@ -602,7 +623,7 @@ def headline(args, dev):
     launch duration."""
     import torch
 
-    w, flops, layers, outs, run = prefill_setup(3, dev)
+    w, flops, nbytes, layers, outs, run = prefill_setup(3, dev)
     L = w.n_layers
     s = torch.cuda.current_stream()
     t_end = time.perf_counter() + args.prewarm
@@ -624,7 +645,7 @@ def headline(args, dev):
            "tokens": tokens, "resource_rows": int(w.cu_len[-1]),
            "roofline": roofline("attn_mfma_kernel<128, attend>", "mfma", flops / L, ms / L,
                                 traffic=measured_traffic(PREFILL_TRAFFIC[3]),
-                                launches=args.steps * L)}
+                                launches=args.steps * L, algorithmic_bytes=nbytes)}
     del layers, outs
     torch.cuda.empty_cache()
     return res
@@ -643,10 +664,14 @@ def main():
     ap.add_argument("--skip-headline", action="store_true",
                     help="run only the rows (for counter collection on one row)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-plan", action="store_true",
+                    help="attend without the per-batch work order (grid in request order)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain elementwise copy (int32 negation, reads and writes "
                          "MIB MiB) 5 times: the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
+    global USE_PLAN
+    USE_PLAN = not args.no_plan
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(sharding is design-only); run with --gpus 1", file=sys.stderr)

@@ -287,6 +287,13 @@ size_t recache_attend_workspace_bytes(int n_req, int max_q, int max_ctx, int max
  *   Tq_b must also not exceed max_q: the prefill grid is sized by it, and
  *       rows past it are written as NaN; with max_q = 1 every request must
  *       have exactly one query (decode writes NaN for one that has more)
+ *   plan: NULL, or the work order that recache_attend_plan built for this
+ *       batch (the same n_req, n_kv_heads and n_q_heads); used by the bf16
+ *       kernels (prefill and decode), ignored by fp32.  It only changes
+ *       which grid position computes which (request, group): the results
+ *       are bit-identical with and without it.  A plan of another batch
+ *       leaves every access in bounds but computes some pairs twice and
+ *       others not at all.
  *   workspace: device scratch of recache_attend_workspace_bytes(...) bytes
  *       (may be NULL when that is 0); contents need no initialisation.
  */
@@ -297,8 +304,35 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
                           int res_rows, const int32_t* cu_kept, const int32_t* res_off,
                           const int32_t* route_off, const int32_t* route_res,
-                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream);
+                          const int32_t* route_tokens, const int32_t* plan, void* out,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Work order of recache_attend_cached's kernels for every layer of a batch.
+ * A schedule, not a passage of the paper: routed resources (Sec. 3,
+ * "Structural Pruning") give the (request, KV group) pairs key streams of
+ * unequal length, and a grid that takes them in request order ends on a
+ * tail of long streams (decode) or loads some XCDs more than others
+ * (prefill).  For each layer l the pairs p = b * n_kv_heads + g are sorted
+ * by their work (longest first; the work counts the 64-key tiles of every
+ * query tile of the prefill kernel, plus a fixed cost per tile, from Tq_b,
+ * Tc_b and route_tokens), and the sorted pairs are dealt row by row to the
+ * n_kv_heads grid positions, alternating direction.
+ *   cu_q/cu_ctx[n_req + 1], route_tokens[n_req][n_layers][n_kv_heads]: as
+ *       for recache_attend_cached (route_tokens from recache_build_routes)
+ *   plan[n_layers][n_req * n_kv_heads] int32 (device), of
+ *       recache_attend_plan_bytes(...) bytes: written, a permutation of
+ *       0 .. n_req * n_kv_heads - 1 per layer.
+ * Build it once per batch, after recache_build_routes; in decode it stays a
+ * valid order as the contexts grow (only its balance ages).
+ * Errors: RECACHE_EINVAL for bad sizes or null pointers;
+ * RECACHE_EUNSUPPORTED when n_req * n_kv_heads exceeds 8192 (pass plan =
+ * NULL to recache_attend_cached then).
+ */
+size_t recache_attend_plan_bytes(int n_req, int n_layers, int n_kv_heads);
+int recache_attend_plan(int n_layers, int n_req, int n_q_heads, int n_kv_heads,
+                        const int32_t* cu_q, const int32_t* cu_ctx,
+                        const int32_t* route_tokens, int32_t* plan, void* stream);
 
 /*
  * recache_attend_cached for callers that cannot allocate device memory: code
@@ -331,8 +365,8 @@ int recache_attend_cached_noalloc(int dtype, int layer, int n_layers, int n_req,
                                   int ctx_rows, const void* res_k, const void* res_v, int res_rows,
                                   const int32_t* cu_kept, const int32_t* res_off,
                                   const int32_t* route_off, const int32_t* route_res,
-                                  const int32_t* route_tokens, void* out, float* lse,
-                                  void* stream);
+                                  const int32_t* route_tokens, const int32_t* plan, void* out,
+                                  float* lse, void* stream);
 
 /*
  * [host] Structural budget selection (Sec. 3, "Structural Pruning").  From

@@ -5,6 +5,7 @@
 // block and enqueues the kernels on the caller's stream.  No device memory is
 // allocated here and nothing synchronises.
 #include <math.h>
+#include <stdint.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -433,8 +434,9 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
                           const void* ctx_v, int ctx_rows, const void* res_k, const void* res_v,
                           int res_rows, const int32_t* cu_kept, const int32_t* res_off,
                           const int32_t* route_off, const int32_t* route_res,
-                          const int32_t* route_tokens, void* out, float* lse, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          const int32_t* route_tokens, const int32_t* plan, void* out,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+    REQUIRE(((uintptr_t)plan & 3) == 0, RECACHE_EINVAL, "plan is not 4-byte aligned");
     int rc_ = check_attend(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q, max_ctx,
                            max_route_len, n_q_heads, n_kv_heads, head_dim, softmax_scale, q, ctx_k,
                            ctx_v, ctx_rows, res_k, res_v, res_rows, cu_kept, res_off, route_off,
@@ -510,6 +512,7 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
         a.cu_kept = cu_kept;
         a.ws_o = static_cast<float*>(workspace);
         a.ws_ml = a.ws_o + (size_t)n_req * n_q_heads * n_splits * head_dim;
+        a.plan = plan;
         return hip_status(launch_decode(a, s), "attend (decode) launch");
     }
     AttnArgs a{};
@@ -538,7 +541,40 @@ int recache_attend_cached(int dtype, int layer, int n_layers, int n_req, const i
     a.route_off = route_off;
     a.route_res = route_res;
     a.cu_kept = cu_kept;
+    a.plan = plan;
     return hip_status(launch_attn_mfma(a, false, head_dim, s), "attend (prefill) launch");
+}
+
+size_t recache_attend_plan_bytes(int n_req, int n_layers, int n_kv_heads) {
+    if (n_req < 1 || n_layers < 1 || n_kv_heads < 1) return 0;
+    return (size_t)n_layers * n_req * n_kv_heads * sizeof(int32_t);
+}
+
+int recache_attend_plan(int n_layers, int n_req, int n_q_heads, int n_kv_heads,
+                        const int32_t* cu_q, const int32_t* cu_ctx, const int32_t* route_tokens,
+                        int32_t* plan, void* stream) {
+    REQUIRE(n_layers >= 1 && n_req >= 1 && n_kv_heads >= 1 && n_q_heads >= n_kv_heads &&
+                n_q_heads % n_kv_heads == 0,
+            RECACHE_EINVAL, "n_layers %d, n_req %d, n_q_heads %d, n_kv_heads %d", n_layers, n_req,
+            n_q_heads, n_kv_heads);
+    REQUIRE((long long)n_req * n_kv_heads <= kMaxPlanPairs, RECACHE_EUNSUPPORTED,
+            "n_req * n_kv_heads = %lld pairs, more than the %d one plan sorts",
+            (long long)n_req * n_kv_heads, kMaxPlanPairs);
+    REQUIRE((long long)n_req * n_layers * n_kv_heads < 0x7fffffffLL, RECACHE_EINVAL,
+            "plan would overflow int32 indexing");
+    REQUIRE(cu_q && cu_ctx && route_tokens && plan, RECACHE_EINVAL, "null pointer argument");
+    REQUIRE(((uintptr_t)plan & 3) == 0, RECACHE_EINVAL, "plan is not 4-byte aligned");
+    PlanArgs a{};
+    a.n_req = n_req;
+    a.n_layers = n_layers;
+    a.n_kv_heads = n_kv_heads;
+    a.wg_rows = attend_block_rows(n_q_heads / n_kv_heads);
+    a.cu_q = cu_q;
+    a.cu_ctx = cu_ctx;
+    a.route_tokens = route_tokens;
+    a.plan = plan;
+    (void)hipGetLastError();
+    return hip_status(launch_attend_plan(a, as_stream(stream)), "recache_attend_plan launch");
 }
 
 }  // extern "C"
@@ -591,8 +627,9 @@ int recache_attend_cached_noalloc(int dtype, int layer, int n_layers, int n_req,
                                   int ctx_rows, const void* res_k, const void* res_v, int res_rows,
                                   const int32_t* cu_kept, const int32_t* res_off,
                                   const int32_t* route_off, const int32_t* route_res,
-                                  const int32_t* route_tokens, void* out, float* lse,
-                                  void* stream) {
+                                  const int32_t* route_tokens, const int32_t* plan, void* out,
+                                  float* lse, void* stream) {
+    REQUIRE(((uintptr_t)plan & 3) == 0, RECACHE_EINVAL, "plan is not 4-byte aligned");
     int rc_ = check_attend(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q, max_ctx,
                            max_route_len, n_q_heads, n_kv_heads, head_dim, softmax_scale, q, ctx_k,
                            ctx_v, ctx_rows, res_k, res_v, res_rows, cu_kept, res_off, route_off,
@@ -612,8 +649,8 @@ int recache_attend_cached_noalloc(int dtype, int layer, int n_layers, int n_req,
     return recache_attend_cached(dtype, layer, n_layers, n_req, cu_q, cu_ctx, total_q, max_q,
                                  max_ctx, max_kv, max_route_len, n_q_heads, n_kv_heads, head_dim,
                                  softmax_scale, q, ctx_k, ctx_v, ctx_rows, res_k, res_v, res_rows,
-                                 cu_kept, res_off, route_off, route_res, route_tokens, out, lse, ws,
-                                 (size_t)RECACHE_NOALLOC_SCRATCH_BYTES, stream);
+                                 cu_kept, res_off, route_off, route_res, route_tokens, plan, out,
+                                 lse, ws, (size_t)RECACHE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int recache_check_offsets(const int32_t* cu, int n, int total, int strict) {

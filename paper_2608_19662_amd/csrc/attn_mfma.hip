@@ -177,12 +177,26 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
     const int jt = a.n_qt - 1 - bid % a.n_qt;
     bid /= a.n_qt;
     const int hq = bid % a.n_hq;
-    const int unit = bid / a.n_hq;
-    // Prefill: the group is rotated by the request, so that an XCD serves
-    // every group over the requests rather than one group throughout; routes
-    // give the groups unequal work, and this evens out the XCDs' shares.
-    // The blocks of one (request, group) still share one XCD.
-    if constexpr (!ENCODE) g = (g + unit) % a.n_kv_heads;
+    int unit = bid / a.n_hq;
+    if constexpr (!ENCODE) {
+        if (a.plan) {
+            // Prefill with a work order: grid position (unit, g) takes the
+            // pair the plan dealt there (longest first, the pairs of one
+            // position balanced across positions, so across the XCDs).
+            const int n_pairs = a.n_units * a.n_kv_heads;
+            int p = a.plan[(size_t)a.layer * n_pairs + unit * a.n_kv_heads + g];
+            p = min(max(p, 0), n_pairs - 1);  // in bounds whatever the plan holds
+            unit = p / a.n_kv_heads;
+            g = p % a.n_kv_heads;
+        } else {
+            // Without one, the group is rotated by the request, so that an
+            // XCD serves every group over the requests rather than one group
+            // throughout; routes give the groups unequal work, and this
+            // evens out the XCDs' shares.
+            g = (g + unit) % a.n_kv_heads;
+        }
+        // either way the blocks of one (request, group) share one XCD
+    }
 
     int q_len, q_row0, off, stream, pos0 = 0;
     int n_seg = 0, s_vis = 0, ctx_row0 = 0, tc = 0;
@@ -722,6 +736,13 @@ constexpr int kAttendWaves = 8;
 // heads x rbw row blocks, hpw the largest power of two up to NW dividing the
 // group size, so every head of the group is covered exactly once.
 template <int NW>
+int block_rows(int ratio) {
+    int h = NW;
+    while (ratio % h) h >>= 1;
+    return 32 * (NW / h);
+}
+
+template <int NW>
 void set_tiling(AttnArgs& b) {
     int h = NW;
     while (b.ratio % h) h >>= 1;
@@ -745,6 +766,8 @@ hipError_t launch(const AttnArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+int attend_block_rows(int ratio) { return ratio >= 1 ? block_rows<kAttendWaves>(ratio) : 0; }
 
 hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream) {
     if (a.ratio < 1 || a.max_rows < 1) return hipErrorInvalidValue;

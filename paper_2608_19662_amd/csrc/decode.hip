@@ -85,11 +85,21 @@ __global__ __launch_bounds__(kThreads, 2) void decode_kernel(const DecodeArgs a)
     int bid = blockIdx.x;
     const int split = bid % a.n_splits;
     bid /= a.n_splits;
-    const int g = bid % a.n_kv_heads;
-    const int b = bid / a.n_kv_heads;
+    int g = bid % a.n_kv_heads;
+    int b = bid / a.n_kv_heads;
+    if (a.plan) {
+        // with a work order the streams run longest first, so that the grid
+        // does not end on a tail of long ones
+        const int n_pairs = a.n_req * a.n_kv_heads;
+        int p = a.plan[(size_t)a.layer * n_pairs + bid];
+        p = min(max(p, 0), n_pairs - 1);  // in bounds whatever the plan holds
+        b = p / a.n_kv_heads;
+        g = p % a.n_kv_heads;
+    }
     const int R = a.ratio;
 
-    // ---- Q^T (B operand), loaded first since it depends on nothing else:
+    // ---- Q^T (B operand), loaded first since it depends on nothing else
+    // (but the pair):
     // lane holds head l16 of the group (zero beyond R), dims ks*32 + grp*8 + [0, 8).
     const int qrow = min(a.cu_q[b], (int)a.lse_rows - 1);
     bf16x8_t qf[T::NKS];

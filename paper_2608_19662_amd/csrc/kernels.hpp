@@ -50,8 +50,12 @@ struct AttnArgs {
     const int32_t* cu_kept;
     const int32_t* res_off;  // route-compacted store rows [n_res * Hkv], or NULL
     int max_rows;            // query rows of the longest unit (the grid covers no more)
+    const int32_t* plan;     // prefill: work order of the (request, group) pairs
+                             // [n_layers][n_units * n_kv_heads], or NULL
 };
 hipError_t launch_attn_mfma(const AttnArgs& a, bool encode, int head_dim, hipStream_t stream);
+// Query rows of one prefill block (32 per row block) for a group size.
+int attend_block_rows(int ratio);
 
 // fp32 reference-precision attention (encode or conversation attend).
 struct AttnF32Args {
@@ -146,9 +150,25 @@ struct DecodeArgs {
     const int32_t* res_off;  // route-compacted store rows [n_res * Hkv], or NULL
     float* ws_o;   // [n_req][Hq][n_splits][head_dim]
     float* ws_ml;  // [n_req][Hq][n_splits][2]  (max in log2 units, sum)
+    const int32_t* plan;  // work order of the (request, group) pairs, or NULL
 };
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 size_t decode_workspace_bytes(int n_req, int n_q_heads, int head_dim, int n_splits);
 int decode_splits(int n_req, int n_kv_heads, int max_kv);
+
+// Work order of the attend kernels (plan.hip): per layer, the pairs
+// b * n_kv_heads + g sorted by their work, longest first, dealt in snake order
+// over the n_kv_heads grid positions.
+constexpr int kMaxPlanPairs = 8192;  // n_req * n_kv_heads per plan (sorted in LDS)
+constexpr int kPlanBlockCost = 3;    // fixed cost of a block, in 64-key tiles
+struct PlanArgs {
+    int n_req, n_layers, n_kv_heads;
+    int wg_rows;  // query rows per prefill block (attend_block_rows)
+    const int32_t* cu_q;
+    const int32_t* cu_ctx;
+    const int32_t* route_tokens;  // [n_req][n_layers][n_kv_heads]
+    int32_t* plan;                // [n_layers][n_req * n_kv_heads]
+};
+hipError_t launch_attend_plan(const PlanArgs& a, hipStream_t stream);
 
 }  // namespace rc

@@ -48,11 +48,14 @@ _SIGS = {
     "recache_attend_cached": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_int,
                                _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p, _c_p, _c_p,
                                _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
-                               _c_p, _c_p, _c_size, _c_p], _c_int),
+                               _c_p, _c_p, _c_p, _c_size, _c_p], _c_int),
+    "recache_attend_plan_bytes": ([_c_int, _c_int, _c_int], _c_size),
+    "recache_attend_plan": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p, _c_p],
+                            _c_int),
     "recache_attend_cached_noalloc": ([_c_int, _c_int, _c_int, _c_int, _c_p, _c_p, _c_int, _c_int,
                                        _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _c_flt, _c_p,
                                        _c_p, _c_p, _c_int, _c_p, _c_p, _c_int, _c_p, _c_p, _c_p,
-                                       _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
+                                       _c_p, _c_p, _c_p, _c_p, _c_p, _c_p], _c_int),
     "recache_select_routes": ([_c_int, _c_int, _c_p, _c_p, _c_int, _c_int, _c_p, _c_p, _c_p, _c_p,
                                _c_p, _c_p], _c_int),
     "recache_check_offsets": ([_c_p, _c_int, _c_int, _c_int], _c_int),
@@ -341,18 +344,28 @@ def attend_workspace_bytes(n_req, max_q, max_ctx, max_kv, n_q_heads, n_kv_heads,
                                                     n_kv_heads, head_dim))
 
 
-def route_len_bound(req_res_off) -> int:
-    """[host] max_route_len for recache_attend_cached: the most resources any
-    request lists (a host copy of req_res_off), which bounds every route list."""
-    a = np.asarray(req_res_off, dtype=np.int64)
-    return int(np.diff(a).max()) if len(a) > 1 else 0
+def attend_plan_bytes(n_req: int, n_layers: int, n_kv_heads: int) -> int:
+    return int(lib().recache_attend_plan_bytes(n_req, n_layers, n_kv_heads))
+
+
+def attend_plan(cu_q, cu_ctx, route_tokens, n_layers: int, n_q_heads: int, n_kv_heads: int, plan,
+                stream=None):
+    """Work order of the attend kernels for every layer of a batch (int32
+    plan[n_layers][n_req * n_kv_heads]); pass it as attend_cached(plan=...)."""
+    n_req = cu_q.numel() - 1
+    _numel(cu_ctx, "cu_ctx", n_req + 1)
+    _numel(route_tokens, "route_tokens", n_req * n_layers * n_kv_heads)
+    _shape(plan, "plan", n_layers, n_req * n_kv_heads)
+    _call("recache_attend_plan", n_layers, n_req, n_q_heads, n_kv_heads,
+          _dev(cu_q, "cu_q", _i32()), _dev(cu_ctx, "cu_ctx", _i32()),
+          _dev(route_tokens, "route_tokens", _i32()), _dev(plan, "plan", _i32()), _stream(stream))
 
 
 def _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu_kept, route_off,
                  route_res, route_tokens, layer, n_layers, out, max_route_len, lse, max_kv,
-                 softmax_scale, res_off):
+                 softmax_scale, res_off, plan):
     """Checked C arguments shared by the two attend entry points, up to
-    route_tokens / out / lse (the caller appends the rest)."""
+    plan / out / lse (the caller appends the rest)."""
     total_q, Hq, d = q.shape
     Hkv = ctx_k.shape[0]
     n_req = cu_q.numel() - 1
@@ -367,6 +380,7 @@ def _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu
     _numel(cu_ctx, "cu_ctx", n_req + 1)
     _numel(route_off, "route_off", E + 1)
     _numel(route_tokens, "route_tokens", E)
+    _shape(plan, "plan", n_layers, n_req * Hkv)
     if res_off is not None:
         _numel(res_off, "res_off", n_res * Hkv + 1)
         if res_k.dim() != 2 or res_k.shape[1] != d:
@@ -385,7 +399,8 @@ def _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu
             _dev(ctx_v, "ctx_v"), ctx_k.shape[1], _dev(res_k, "res_k"), _dev(res_v, "res_v"),
             res_rows, _dev(cu_kept, "cu_kept", _i32()), _dev(res_off, "res_off", _i32()),
             _dev(route_off, "route_off", _i32()), _dev(route_res, "route_res", _i32()),
-            _dev(route_tokens, "route_tokens", _i32()), _dev(out, "out"), _dev(lse, "lse"))
+            _dev(route_tokens, "route_tokens", _i32()), _dev(plan, "plan", _i32()),
+            _dev(out, "out"), _dev(lse, "lse"))
 
 
 def route_len_bound(req_res_off) -> int:
@@ -398,16 +413,17 @@ def route_len_bound(req_res_off) -> int:
 def attend_cached(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k, res_v, cu_kept,
                   route_off, route_res, route_tokens, layer: int, n_layers: int, out, *,
                   max_route_len: int, lse=None, workspace=None, max_kv: int = 0,
-                  softmax_scale: float = 0.0, res_off=None, stream=None):
+                  softmax_scale: float = 0.0, res_off=None, plan=None, stream=None):
     """Conversation queries over routed kept resource rows + causal context (one layer).
 
     res_k / res_v are [Hkv][rows][d] kept rows, or with res_off (this layer's
     row of a store table) a route-compacted store [rows][d].  max_route_len
     bounds the resources of every route list (route_len_bound of the request
-    lists; at most 1024)."""
+    lists; at most 1024).  plan, from attend_plan for this batch, only
+    reorders the grid (results bit-identical)."""
     args = _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu_kept,
                         route_off, route_res, route_tokens, layer, n_layers, out, max_route_len,
-                        lse, max_kv, softmax_scale, res_off)
+                        lse, max_kv, softmax_scale, res_off, plan)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("recache_attend_cached", *args, _dev(workspace, "workspace"), ws_bytes, _stream(stream))
 
@@ -415,13 +431,13 @@ def attend_cached(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k
 def attend_cached_noalloc(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q: int, max_ctx: int, res_k, res_v,
                           cu_kept, route_off, route_res, route_tokens, layer: int, n_layers: int,
                           out, *, max_route_len: int, lse=None, max_kv: int = 0,
-                          softmax_scale: float = 0.0, res_off=None, stream=None):
+                          softmax_scale: float = 0.0, res_off=None, plan=None, stream=None):
     """attend_cached without a workspace: decode's split partials live in the
     library's static per-GPU scratch (see recache.h: calls that overlap on one
     GPU race)."""
     args = _attend_args(q, ctx_k, ctx_v, cu_q, cu_ctx, max_q, max_ctx, res_k, res_v, cu_kept,
                         route_off, route_res, route_tokens, layer, n_layers, out, max_route_len,
-                        lse, max_kv, softmax_scale, res_off)
+                        lse, max_kv, softmax_scale, res_off, plan)
     _call("recache_attend_cached_noalloc", *args, _stream(stream))
 
 

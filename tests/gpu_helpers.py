@@ -109,8 +109,16 @@ class Routes:
                                       w.n_kv_heads, w.head_dim)
         return torch.empty(max(n, 4) // 4, dtype=torch.float32, device=DEV) if n else None
 
+    def plan(self, stream=None):
+        """GPU-built work order of every layer, [L][n_req * Hkv]."""
+        w = self.w
+        p = torch.empty(w.n_layers, w.n_req * w.n_kv_heads, dtype=torch.int32, device=DEV)
+        rc.attend_plan(self.cu_q, self.cu_ctx, self.route_tokens, w.n_layers, w.n_q_heads,
+                       w.n_kv_heads, p, stream=stream)
+        return p
+
     def attend(self, q, ck, cv, rk, rv, layer, lse=True, workspace=None, max_kv=0, stream=None,
-               res_off=None):
+               res_off=None, plan=None):
         w = self.w
         out = torch.empty_like(q)
         l = torch.empty(w.n_q_heads, q.shape[0], dtype=torch.float32, device=DEV) if lse else None
@@ -118,8 +126,9 @@ class Routes:
                          self.cu_rows, self.route_off, self.route_res, self.route_tokens, layer,
                          w.n_layers, out, lse=l, workspace=workspace, max_kv=max_kv,
                          max_route_len=max(self.max_route_len, 1), stream=stream,
-                         res_off=res_off)
+                         res_off=res_off, plan=plan)
         return out, l
+
 
     def store_offsets(self):
         """GPU-built row tables of the route-compacted store, [L][n_res * G + 1]."""
@@ -128,3 +137,38 @@ class Routes:
                           device=DEV)
         rc.route_store_offsets(self.mask, self.cu_rows, off, total_kept=int(w.cu_rows[-1]))
         return off
+
+
+def plan_reference(cu_q, cu_ctx, route_tokens, n_layers, n_q_heads, n_kv_heads):
+    """The work order the plan builder documents, in plain Python: per layer
+    the pairs b * G + g sorted by (work descending, pair ascending), the
+    k-th sorted pair at grid row k // G, position k % G (even rows) or
+    G - 1 - k % G (odd rows).  Work: for every prefill query tile of wg
+    rows, its 64-key tiles (keys up to its last row) plus 3."""
+    G = n_kv_heads
+    ratio = n_q_heads // G
+    h = 8
+    while ratio % h:
+        h //= 2
+    wg = 32 * (8 // h)
+    cu_q = np.asarray(cu_q, np.int64)
+    cu_ctx = np.asarray(cu_ctx, np.int64)
+    n_req = len(cu_q) - 1
+    tok = np.asarray(route_tokens, np.int64).reshape(n_req, n_layers, G)
+    out = np.zeros((n_layers, n_req * G), np.int32)
+    for l in range(n_layers):
+        work = []
+        for b in range(n_req):
+            tq = int(cu_q[b + 1] - cu_q[b])
+            tc = int(cu_ctx[b + 1] - cu_ctx[b])
+            for g in range(G):
+                off = int(tok[b, l, g]) + tc - tq
+                wk = 0
+                for r0 in range(0, max(tq, 0), wg):
+                    wk += max(off + min(r0 + wg, tq) - 1, 0) // 64 + 1 + 3
+                work.append(min(wk, 2 ** 31 - 1))
+        order = sorted(range(n_req * G), key=lambda i: (-work[i], i))
+        for k, pair in enumerate(order):
+            row, c = divmod(k, G)
+            out[l, row * G + (G - 1 - c if row % 2 else c)] = pair
+    return out

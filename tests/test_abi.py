@@ -94,8 +94,8 @@ def att(**kw):
     a = dict(dtype=1, layer=0, n_layers=36, n_req=2, cu_q=FAKE, cu_ctx=FAKE, total_q=2, max_q=1,
              max_ctx=16, max_kv=0, max_route_len=32, Hq=32, Hkv=8, d=128, scale=0.0, q=FAKE,
              ck=FAKE, cv=FAKE, ctx_rows=32, rk=FAKE, rv=FAKE, res_rows=8, cu_kept=FAKE,
-             res_off=None, route_off=FAKE, route_res=FAKE, route_tokens=FAKE, out=FAKE, lse=None,
-             ws=None, ws_bytes=0, stream=None)
+             res_off=None, route_off=FAKE, route_res=FAKE, route_tokens=FAKE, plan=None, out=FAKE,
+             lse=None, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return rc.lib().recache_attend_cached(*a.values())
 
@@ -112,6 +112,7 @@ def att(**kw):
     (dict(route_res=None), rc.EINVAL),
     (dict(ws=None), rc.EWORKSPACE),       # decode needs split-KV scratch
     (dict(ws=FAKE, ws_bytes=16), rc.EWORKSPACE),
+    (dict(plan=FAKE + 2), rc.EINVAL),     # a plan is int32
 ])
 def test_attend_rejects(kw, code):
     assert att(**kw) == code
@@ -251,10 +252,27 @@ def test_noalloc_rejects_partials_beyond_the_scratch():
     assert need > 32 * 1024 * 1024
     code = L.recache_attend_cached_noalloc(1, 0, 1, 4096, FAKE, FAKE, 4096, 1, 64, 0, 4, 64, 8,
                                            128, 0.0, FAKE, FAKE, FAKE, 64, FAKE, FAKE, 8, FAKE, None,
-                                           FAKE, FAKE, FAKE, FAKE, None, None)
+                                           FAKE, FAKE, FAKE, None, FAKE, None, None)
     assert code == rc.EWORKSPACE
     assert "static scratch" in rc.last_error()
     # and the ordinary argument checks come first
     assert L.recache_attend_cached_noalloc(1, 5, 1, 4096, FAKE, FAKE, 4096, 1, 64, 0, 4, 64, 8,
                                            128, 0.0, FAKE, FAKE, FAKE, 64, FAKE, FAKE, 8, FAKE,
-                                           None, FAKE, FAKE, FAKE, FAKE, None, None) == rc.EINVAL
+                                           None, FAKE, FAKE, FAKE, None, FAKE, None, None) == rc.EINVAL
+
+
+def test_attend_plan_sizes_and_checks():
+    """The work-order builder: its size, and its host checks (no HIP call)."""
+    L = rc.lib()
+    assert rc.attend_plan_bytes(8, 36, 8) == 36 * 8 * 8 * 4
+    assert rc.attend_plan_bytes(0, 36, 8) == 0
+    # n_layers, n_req, n_q_heads, n_kv_heads, cu_q, cu_ctx, route_tokens, plan, stream
+    assert L.recache_attend_plan(36, 8, 32, 8, FAKE, FAKE, FAKE, None, None) == rc.EINVAL
+    assert "null" in rc.last_error()
+    assert L.recache_attend_plan(0, 8, 32, 8, FAKE, FAKE, FAKE, FAKE, None) == rc.EINVAL
+    assert L.recache_attend_plan(36, 8, 30, 8, FAKE, FAKE, FAKE, FAKE, None) == rc.EINVAL
+    assert L.recache_attend_plan(36, 8, 32, 8, FAKE, FAKE, FAKE, FAKE + 1, None) == rc.EINVAL
+    assert "aligned" in rc.last_error()
+    # more pairs than one plan sorts in LDS
+    assert L.recache_attend_plan(1, 1025, 32, 8, FAKE, FAKE, FAKE, FAKE, None) == rc.EUNSUPPORTED
+    assert "8192" in rc.last_error()

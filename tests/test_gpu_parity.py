@@ -374,7 +374,11 @@ def run_attend_case(w, layer, chain=False):
     max_kv = rt.max_kv(layer)
     ws = rt.workspace(max_kv)
     out, lse = rt.attend(q, ck, cv, grk, grv, layer, workspace=ws, max_kv=max_kv)
+    # the work order only moves pairs between grid positions: bit-identical
+    pout, plse = rt.attend(q, ck, cv, grk, grv, layer, workspace=ws, max_kv=max_kv, plan=rt.plan())
     torch.cuda.synchronize()
+    assert torch.equal(pout, out), "attend with a work order differs"
+    assert torch.equal(plse, lse), "attend lse with a work order differs"
     if chain:
         rout, rlse = oracle.attend(q.cpu(), ck.cpu(), cv.cpu(), w.cu_q, w.cu_ctx, rk.cpu(), rv.cpu(),
                                    w.cu_len, w.req_res_off, w.req_res, w.mask, layer,
