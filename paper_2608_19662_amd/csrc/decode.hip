@@ -437,7 +437,7 @@ hipError_t launch_dec(const DecodeArgs& a, hipStream_t s) {
 
 int decode_splits(int n_req, int n_kv_heads, int max_kv) {
     const long units = (long)n_req * n_kv_heads;
-    long s = (2048 + units - 1) / units;       // about four rounds of two blocks per CU
+    long s = (1536 + units - 1) / units;       // about three rounds of two blocks per CU
     const long by_len = (max_kv + 511) / 512;  // and at least ~512 keys per block
     if (s > by_len) s = by_len;
     if (s > 64) s = 64;
