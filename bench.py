@@ -20,8 +20,8 @@ resources each plus 4096 context rows), the kept-row gather, the route build,
 a shared-prefix encode, a route-compacted store and the Dense baselines.
 
 Inputs are synthetic (seeded N(0, 1) tensors, see workloads.py) and resident
-in HBM before timing starts.  The CPU baseline is the fp64 oracle on half of
-one layer of the headline workload, extrapolated to the 36-layer step.
+in HBM before timing starts.  The CPU baseline is the fp64 oracle on one
+layer of the headline workload, extrapolated to the 36-layer step.
 """
 from __future__ import annotations
 
@@ -584,12 +584,12 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(dev, n_req=4):
+def cpu_baseline(dev, n_req=8):
     """The fp64 oracle on a bounded sample of the headline workload: every
-    query row and head of the first n_req requests of layer 0 (about half a
-    layer, 15-20 s on 16 host threads), timed once.  The 36-layer step is
-    extrapolated from the sample's share of the step's pairs (the layers of
-    this workload have identical structure)."""
+    query row and head of the first n_req requests of layer 0 (by default
+    all 8, one whole layer: about 35 s on 16 host threads), timed once.  The
+    36-layer step is extrapolated from the sample's share of the step's pairs
+    (the layers of this workload have identical structure)."""
     import oracle
     from paper_2608_19662_amd.workloads import config
 
@@ -736,7 +736,7 @@ def main():
         return
     cpu = None
     if not args.no_cpu_baseline:
-        log("cpu baseline (oracle, half of one config 3 layer)")
+        log("cpu baseline (oracle, one config 3 layer)")
         cpu = cpu_baseline(dev)
         log("  ", json.dumps(cpu))
     w = h["w"]
