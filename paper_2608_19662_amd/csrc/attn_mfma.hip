@@ -14,10 +14,10 @@
 // off = S_vis + Tc - Tq.  Both are a list of segments followed by a causal
 // part, and share one code path.
 //
-// Work decomposition.  A workgroup is 4 waves that share one KV group and
-// four (query head, 32-row block) pairs of it (hpw heads x rbw row blocks,
-// hpw the largest of 4, 2, 1 dividing the group size); each wave owns one
-// pair and computes the transposed products
+// Work decomposition.  A workgroup is NW waves (4 in encode, 8 in prefill)
+// that share one KV group and NW (query head, 32-row block) pairs of it (hpw
+// heads x rbw row blocks, hpw the largest power of two up to NW dividing the
+// group size); each wave owns one pair and computes the transposed products
 //     S^T = K Q^T    (32x32x16 bf16 MFMA; A = K rows from LDS, B = Q^T in VGPRs)
 //     O^T += V^T P^T (A = V^T from LDS, B = P^T straight from the S^T accumulators)
 // so that each lane owns exactly one query row in both accumulators: row max
