@@ -34,10 +34,14 @@
 // in the key order in which the S^T accumulator hands P^T to the second
 // product.
 //
+// Softmax.  Weights are formed against a reference max per row, set by the
+// first tile and moved only when a weight could grow past 2^16, so that the
+// common tile needs no row max before its exponentials.
+//
 // Output.  The normalised rows go through LDS and leave as whole rows, four
-// 256-byte rows per 16-byte store instruction.  Values the loop does not use
-// (the lane index, the rescale threshold) are not held across it, so that the
-// registers spilled around the last tiles stay few.
+// 256-byte rows per 16-byte store instruction.  The lane index is not held
+// across the loop, so that the registers spilled around the last tiles stay
+// few.
 //
 // Tiles never cross a resource boundary in encode, and the reduction order
 // depends only on local indices, so a resource's outputs are bit-identical
@@ -555,7 +559,6 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
     __syncthreads();  // every wave has read K(0) before K(2) is copied over it
 
     const float sl2 = a.scale_log2;
-    const float lazy = a.lazy;
     const bf16x2 ones2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0) in bf16
     float m = -INFINITY;   // running max of raw logits for this lane's row
     float lsum = 0.f;      // this lane's partial sum of the (bf16-rounded) weights
@@ -586,42 +589,41 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
                 for (int r = 0; r < 16; ++r)
                     if (kb * 32 + (r >> 2) * 8 + (r & 3) > rem) sc[kb][r] = -INFINITY;
         }
-        float mt = fmaxf(sc[0][0], sc[0][1]);
+        auto row_max = [&]() {
+            float mt = fmaxf(sc[0][0], sc[0][1]);
 #pragma unroll
-        for (int r = 2; r < 16; ++r) mt = fmaxf(mt, sc[0][r]);
+            for (int r = 2; r < 16; ++r) mt = fmaxf(mt, sc[0][r]);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sc[1][r]);
-        mt = pair_max(mt);
-        // Lazy rescale: weights are taken relative to m, which only moves
-        // when a logit exceeds it by more than 8 / sl2 (weights stay <= 2^8,
-        // far from overflow); O and the row sum share m, so the result is
-        // exact.
-        if (__builtin_amdgcn_ballot_w64(mt > m + lazy)) {
-            const float m_new = fmaxf(m, mt);
-            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
-            lsum *= alpha;
-#pragma unroll
-            for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
-            m = m_new;
-        }
+            for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sc[1][r]);
+            return pair_max(mt);
+        };
+        // the first tile sets the reference m (O and the row sum are still 0)
+        if (kt == 0) m = row_max();
         // S(t + 1) on the matrix pipe while the weights of tile t are formed.
         if constexpr (NEXT) qk(sacc[cur ^ 1], cur ? k_st0 : k_st1);
-        const float msl = m * sl2;
+        // Weights relative to the reference m as it stands (no max of the
+        // tile first), with this lane's sum of them as rounded for the P V
+        // product, so that the output is an exact weighted mean of the V rows
+        // it used.
         bf16x8 pf[4];
+        float tsum;
+        auto weights = [&]() {
+            const float msl = m * sl2;
+            tsum = 0.f;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            uint32_t w[4];
+            for (int s = 0; s < 4; ++s) {
+                uint32_t w[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][8 * (s & 1) + 2 * i], sl2, -msl));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][8 * (s & 1) + 2 * i + 1], sl2, -msl));
-                w[i] = pack_bf16x2(p0, p1);
-                // row sum of the weights as rounded for the P V product, so
-                // the output is an exact weighted mean of the V rows it used
-                lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[i]), ones2, lsum, false);
+                for (int i = 0; i < 4; ++i) {
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][8 * (s & 1) + 2 * i], sl2, -msl));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][8 * (s & 1) + 2 * i + 1], sl2, -msl));
+                    w[i] = pack_bf16x2(p0, p1);
+                    tsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[i]), ones2, tsum, false);
+                }
+                pf[s] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
             }
-            pf[s] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-        }
+        };
+        weights();
         if constexpr (NEXT) {
             // Interleave: K reads two MFMAs ahead, then each MFMA of S(t + 1)
             // followed by an equal share of the ~96 VALU instructions that
@@ -637,6 +639,22 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        // The reference m stays until a weight could exceed 2^16, which
+        // shows as a lane's sum of them above that (or not finite, for a
+        // logit more than 128 / sl2 above m).  Then m becomes the larger of
+        // m and the tile's row max, O and the row sum are rescaled by the
+        // change, and the tile's weights are formed again.  O and the row
+        // sum always share m, so the result is exact whatever m is.
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(tsum <= 65536.0f)) != 0, 0)) {
+            const float m_new = fmaxf(m, row_max());
+            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
+            lsum *= alpha;
+#pragma unroll
+            for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
+            m = m_new;
+            weights();
+        }
+        lsum += tsum;
         const char* st = cur ? v_st1 : v_st0;
 #pragma unroll
         for (int db = 0; db < TL::NDB; ++db) {
@@ -756,7 +774,6 @@ template <int HD, bool ENCODE, int NW>
 hipError_t launch(const AttnArgs& a, hipStream_t stream) {
     AttnArgs b = a;
     set_tiling<NW>(b);
-    b.lazy = 8.0f / a.scale_log2;
     const long blocks = (long)b.n_qt * b.n_units * b.n_hq * b.n_kv_heads;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;

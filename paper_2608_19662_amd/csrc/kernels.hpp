@@ -21,7 +21,6 @@ struct AttnArgs {
     int n_units;  // resources (encode) or requests (prefill)
     int n_qt;     // query tiles per unit (ceil(max_rows / (32 * rbw)))
     float scale_log2;  // softmax_scale * log2(e)
-    float lazy;        // rescale threshold 8 / scale_log2 (set by the launch)
     const uint16_t* q;
     uint16_t* out;
     float* lse;
