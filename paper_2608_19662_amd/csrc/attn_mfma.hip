@@ -560,7 +560,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
 
     const float sl2 = a.scale_log2;
     const bf16x2 ones2 = __builtin_bit_cast(bf16x2, 0x3F803F80u);  // (1.0, 1.0) in bf16
-    float m = -INFINITY;   // running max of raw logits for this lane's row
+    float m = -INFINITY;   // reference max of raw logits for this lane's row (set by the first tile)
     float lsum = 0.f;      // this lane's partial sum of the (bf16-rounded) weights
     // keys p <= off + my_q are visible to this lane's row; this lane's S^T
     // entries of a tile start at key offset half * 4
@@ -647,7 +647,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
         // sum always share m, so the result is exact whatever m is.
         if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(tsum <= 65536.0f)) != 0, 0)) {
             const float m_new = fmaxf(m, row_max());
-            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);  // 0 when m == -inf
+            const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);
             lsum *= alpha;
 #pragma unroll
             for (int db = 0; db < TL::NDB; ++db) oacc[db] *= alpha;
