@@ -66,6 +66,8 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 constexpr int kBK = 64;  // keys per tile
+// A lane's sum of a tile's weights above this moves the reference max.
+constexpr float kWeightCap = 65536.0f;  // 2^16
 constexpr int kMaxSeg = 1024;
 // Third dword of a gfx9 buffer resource for raw (unformatted) loads.
 constexpr int kBufferFlags = 0x00020000;
@@ -643,9 +645,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_mfma_kernel(const AttnAr
         // shows as a lane's sum of them above that (or not finite, for a
         // logit more than 128 / sl2 above m).  Then m becomes the larger of
         // m and the tile's row max, O and the row sum are rescaled by the
-        // change, and the tile's weights are formed again.  O and the row
-        // sum always share m, so the result is exact whatever m is.
-        if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(tsum <= 65536.0f)) != 0, 0)) {
+        // change, and the tile's weights are formed again (each at most 1
+        // now).  O and the row sum always share m, so the result is exact
+        // whatever m is.
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(tsum <= kWeightCap)) != 0, 0)) {
             const float m_new = fmaxf(m, row_max());
             const float alpha = __builtin_amdgcn_exp2f((m - m_new) * sl2);
             lsum *= alpha;
