@@ -27,23 +27,25 @@ def ramp(n, step, dtype):
     return (step * torch.arange(n, dtype=torch.float32)).to(dtype)
 
 
-def test_reference_moves_encode():
+@pytest.mark.parametrize("Hq,Hkv,d", [(32, 8, 128), (8, 2, 64), (12, 4, 64)])
+def test_reference_moves_encode(Hq, Hkv, d):
     """Encode: a rising resource with two spikes, a falling one, short ones."""
-    print_case("softmax reference, encode")
+    print_case("softmax reference, encode", Hq, Hkv, d)
     lengths = np.array([700, 300, 129, 65, 1], np.int32)
-    w = EncodeWorkload(seed=61, lengths=lengths, n_q_heads=32, n_kv_heads=8, head_dim=128,
+    w = EncodeWorkload(seed=61, lengths=lengths, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d,
                        dtype="bf16", rope_base=1e6)
     q, k, v = w.tensors("cpu")
-    # dimension 63 pairs with 127 and turns by 1e6^(-63/64) rad per position,
-    # so the large component keeps its sign along a resource
-    q[:, :, 63] = 4.0
+    # dimension d/2 - 1 pairs with d - 1 and turns by 1e6^(-(d - 2)/d) rad per
+    # position, so the large component keeps its sign along a resource
+    c = d // 2 - 1
+    q[:, :, c] = 4.0
     for r, n in enumerate(lengths):
         o = int(w.cu_len[r])
         up = ramp(int(n), 0.5, k.dtype)
-        k[o:o + n, :, 63] = (up if r != 1 else up.flip(0))[:, None]
+        k[o:o + n, :, c] = (up if r != 1 else up.flip(0))[:, None]
     o0 = int(w.cu_len[0])
-    k[o0 + 400, :, 63] = 900.0   # about 360 above the reference in log2 units
-    k[o0 + 450, :, 63] = 1200.0  # and again past the moved reference
+    k[o0 + 400, :, c] = 900.0   # about 360 above the reference in log2 units
+    k[o0 + 450, :, c] = 1200.0  # and again past the moved reference
     out, kc, vc, lse = gpu_encode(w, q.to(DEV), k.to(DEV), v.to(DEV))
     ref = oracle.encode(q, k, v, w.cu_len, w.rope_base)
     check(out, ref["out"], "bf16", "out")
@@ -52,13 +54,14 @@ def test_reference_moves_encode():
     assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
 
 
+@pytest.mark.parametrize("Hq,Hkv,d", [(32, 8, 128), (12, 4, 64)])
 @pytest.mark.parametrize("q_lens,ctx_lens", [([100, 1, 64], [330, 1, 700]),   # prefill
                                              ([1, 1, 1], [300, 1200, 64])])  # decode
-def test_reference_moves_attend(q_lens, ctx_lens):
+def test_reference_moves_attend(q_lens, ctx_lens, Hq, Hkv, d):
     """Prefill and decode over kept resource rows and context rows whose keys
     rise along their buffers, with spikes in both."""
-    print_case("softmax reference, attend", q_lens, ctx_lens)
-    w = small_attend(62, 3, 6, 32, 8, 128, "bf16", q_lens, ctx_lens, max_len=400, mask_p=0.7)
+    print_case("softmax reference, attend", q_lens, ctx_lens, Hq, Hkv, d)
+    w = small_attend(62, 3, 6, Hq, Hkv, d, "bf16", q_lens, ctx_lens, max_len=400, mask_p=0.7)
     layer = 1
     q, ck, cv, rk, rv = w.layer_tensors(layer, DEV, compacted=True)
     q[:, :, 0] = 4.0
