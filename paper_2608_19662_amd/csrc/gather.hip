@@ -8,6 +8,8 @@
 //   - a route-compacted store (both pruning stages): per layer, only the
 //     visible (resource, group) routes hold rows, resource-major, each with
 //     the kept rows of its resource.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -15,20 +17,26 @@ namespace rc {
 
 namespace {
 
-// One block per (resource r, KV head g): the kept rows of r for head g go
-// to rows g * total_kept + cu_kept[r] + j of the compacted caches.  Each
-// thread moves U 16-byte chunks per step, all loads issued before the
-// stores; source rows are clamped into the caches.
+// Blocks per (resource r, KV head g): n_parts of them share the kept rows of
+// r for head g (contiguous, equal shares), which go to rows g * total_kept +
+// cu_kept[r] + j of the compacted caches.  Each thread moves U 16-byte
+// chunks per step, all loads issued before the stores; source rows are
+// clamped into the caches.
 __global__ __launch_bounds__(256) void prune_gather_kernel(
-    int chunks_per_row, int n_kv_heads, const int32_t* __restrict__ cu_len,
+    int chunks_per_row, int n_kv_heads, int n_parts, const int32_t* __restrict__ cu_len,
     const int32_t* __restrict__ cu_kept, const int32_t* __restrict__ kept_idx, long total_T,
     long total_kept, const u32x4* __restrict__ kc, const u32x4* __restrict__ vc,
     u32x4* __restrict__ ko, u32x4* __restrict__ vo) {
-    constexpr int U = 4;
-    const int r = blockIdx.x / n_kv_heads, g = blockIdx.x % n_kv_heads;
-    const long k0 = cu_kept[r];
-    const long k1 = min((long)cu_kept[r + 1], total_kept);
-    if (k0 < 0 || k1 <= k0) return;
+    constexpr int U = 8;
+    const int part = blockIdx.x % n_parts, rg = blockIdx.x / n_parts;
+    const int r = rg / n_kv_heads, g = rg % n_kv_heads;
+    const long r0 = cu_kept[r];
+    const long r1 = min((long)cu_kept[r + 1], total_kept);
+    if (r0 < 0 || r1 <= r0) return;
+    // this block's share of the resource's kept rows
+    const long k0 = r0 + (r1 - r0) * part / n_parts;
+    const long k1 = r0 + (r1 - r0) * (part + 1) / n_parts;
+    if (k1 <= k0) return;
     const long beg = cu_len[r];
     const int sh = __builtin_ctz(chunks_per_row);  // a power of two
     const long n = (k1 - k0) * chunks_per_row;
@@ -168,7 +176,7 @@ __global__ __launch_bounds__(256) void store_routes_kernel(
     const int32_t* __restrict__ kept_idx, long total_T, long total_kept, long store_rows,
     const u32x4* __restrict__ kc, const u32x4* __restrict__ vc, u32x4* __restrict__ ko,
     u32x4* __restrict__ vo) {
-    constexpr int U = 4;
+    constexpr int U = 8;
     const int i = blockIdx.x;
     const int o0 = off[i];
     const int n_rows = off[i + 1] - o0;
@@ -237,10 +245,13 @@ hipError_t launch_prune_gather(int elem_bytes, int n_res, const int32_t* cu_len,
                                long total_kept, int n_kv_heads, int head_dim, const void* k_cache,
                                const void* v_cache, void* k_kept, void* v_kept, hipStream_t s) {
     const int cpr = head_dim * elem_bytes / 16;
-    const long blocks = (long)n_res * n_kv_heads;
-    if (blocks == 0) return hipSuccess;
+    const long rg = (long)n_res * n_kv_heads;
+    if (rg == 0) return hipSuccess;
+    // about 2048 blocks (eight per CU) whatever the resource count
+    const int parts = (int)std::min(16L, std::max(1L, (2048 + rg - 1) / rg));
+    const long blocks = rg * parts;
     if (blocks > 0x7fffffffL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(prune_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr, n_kv_heads,
+    hipLaunchKernelGGL(prune_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, s, cpr, n_kv_heads, parts,
                        cu_len, cu_kept, kept_idx, total_T, total_kept,
                        static_cast<const u32x4*>(k_cache), static_cast<const u32x4*>(v_cache),
                        static_cast<u32x4*>(k_kept), static_cast<u32x4*>(v_kept));
