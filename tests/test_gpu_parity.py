@@ -765,7 +765,9 @@ def test_index_random_cases(seed):
     mask_d = torch.from_numpy(mask).to(DEV)
     E = n_req * L * G
     route_off = torch.empty(E + 1, dtype=torch.int32, device=DEV)
-    route_res = torch.empty(max(1, len(req_res) * L * G), dtype=torch.int32, device=DEV)
+    # capacity for every entry of the req_res passed (one placeholder when all
+    # requests are empty) in every (layer, group)
+    route_res = torch.empty(max(1, len(req_res)) * L * G, dtype=torch.int32, device=DEV)
     route_tokens = torch.empty(E, dtype=torch.int32, device=DEV)
     rc.build_routes(i32(req_res_off), i32(req_res if len(req_res) else [0]), mask_d, i32(cu_kept),
                     route_off, route_res, route_tokens)
