@@ -78,6 +78,7 @@ __global__ __launch_bounds__(256) void route_count_kernel(
     const int l = (int)((e / G) % L);
     const int b = (int)(e / ((long)G * L));
     int cnt = 0, tok = 0;
+#pragma unroll 4
     for (int j = req_res_off[b]; j < req_res_off[b + 1]; ++j) {
         const int r = req_res[j];
         if (r < 0 || r >= n_res) continue;
@@ -91,25 +92,30 @@ __global__ __launch_bounds__(256) void route_count_kernel(
 }
 
 // In-place inclusive scan of route_off[1..E] by one block; route_off[0] = 0.
+// The entries go through in chunks of 4096 consecutive ones, four per thread
+// (coalesced loads and stores), with a block-wide scan of the thread sums per
+// chunk and the chunk totals carried on.
 __global__ __launch_bounds__(1024) void route_scan_kernel(long E, int32_t* __restrict__ route_off) {
-    __shared__ int part[1024];
+    constexpr int V = 4;
+    __shared__ int wave_tot[2][16];  // alternate buffers: one barrier per chunk suffices
     const int tid = threadIdx.x;
-    const long per = (E + 1023) / 1024;
-    const long a = 1 + tid * per, b = a + per < E + 1 ? a + per : E + 1;
-    int s = 0;
-    for (long i = a; i < b; ++i) s += route_off[i];
-    part[tid] = s;
-    __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-        const int add = tid >= o ? part[tid - o] : 0;
-        __syncthreads();
-        part[tid] += add;
-        __syncthreads();
-    }
-    int run = part[tid] - s;
-    for (long i = a; i < b; ++i) {
-        run += route_off[i];
-        route_off[i] = run;
+    int carry = 0, k = 0;
+    for (long base = 1; base <= E; base += 1024L * V, k ^= 1) {
+        const long i0 = base + (long)tid * V;
+        int v[V], s = 0;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            v[j] = i0 + j <= E ? route_off[i0 + j] : 0;
+            s += v[j];
+        }
+        int total;
+        int run = carry + block_exclusive_scan<16>(s, wave_tot[k], &total);
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            run += v[j];
+            if (i0 + j <= E) route_off[i0 + j] = run;
+        }
+        carry += total;
     }
     if (tid == 0) route_off[0] = 0;
 }
@@ -124,6 +130,7 @@ __global__ __launch_bounds__(256) void route_fill_kernel(
     const int l = (int)((e / G) % L);
     const int b = (int)(e / ((long)G * L));
     int w = route_off[e];
+#pragma unroll 4
     for (int j = req_res_off[b]; j < req_res_off[b + 1]; ++j) {
         const int r = req_res[j];
         if (r < 0 || r >= n_res) continue;
