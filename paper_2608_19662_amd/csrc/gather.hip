@@ -140,37 +140,40 @@ __global__ __launch_bounds__(256) void route_fill_kernel(
 
 // One block per layer: exclusive scan over routes i = r * G + g of
 // mask[r][l][g] * kept_r, written to the layer's row of the table, plus the
-// layer's total.  Each thread scans a contiguous run of routes.
+// layer's total.  The routes go through in chunks of 4096 consecutive ones,
+// four per thread, with a block-wide scan of the thread sums per chunk and
+// the chunk totals carried on.
 __global__ __launch_bounds__(1024) void store_offsets_kernel(
     int n_res, int L, int G, const uint8_t* __restrict__ mask,
     const int32_t* __restrict__ cu_kept, int32_t* __restrict__ store_off) {
-    __shared__ int part[1024];
+    constexpr int V = 4;
+    __shared__ int wave_tot[2][16];  // alternate buffers: one barrier per chunk suffices
     const int l = blockIdx.x, tid = threadIdx.x;
     const long n = (long)n_res * G;
     int32_t* off = store_off + (size_t)l * (n + 1);
-    const long per = (n + 1023) / 1024;
-    const long a = tid * per < n ? tid * per : n;
-    const long b = a + per < n ? a + per : n;
     auto rows = [&](long i) {
         const int r = (int)(i / G), g = (int)(i % G);
         return mask[((size_t)r * L + l) * G + g] ? cu_kept[r + 1] - cu_kept[r] : 0;
     };
-    int sum = 0;
-    for (long i = a; i < b; ++i) sum += rows(i);
-    part[tid] = sum;
-    __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-        const int add = tid >= o ? part[tid - o] : 0;
-        __syncthreads();
-        part[tid] += add;
-        __syncthreads();
+    int carry = 0, k = 0;
+    for (long base = 0; base < n; base += 1024L * V, k ^= 1) {
+        const long i0 = base + (long)tid * V;
+        int v[V], s = 0;
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            v[j] = i0 + j < n ? rows(i0 + j) : 0;
+            s += v[j];
+        }
+        int total;
+        int run = carry + block_exclusive_scan<16>(s, wave_tot[k], &total);
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            if (i0 + j < n) off[i0 + j] = run;
+            run += v[j];
+        }
+        carry += total;
     }
-    int run = part[tid] - sum;
-    for (long i = a; i < b; ++i) {
-        off[i] = run;
-        run += rows(i);
-    }
-    if (tid == 1023) off[n] = part[1023];
+    if (tid == 0) off[n] = carry;
 }
 
 // One block per route i = r * G + g of the layer: a visible route copies
