@@ -408,14 +408,48 @@ __global__ __launch_bounds__(HD) void combine_kernel(const DecodeArgs a) {
     const int b = bh / a.n_q_heads, h = bh % a.n_q_heads;
     const int d = threadIdx.x;
     const size_t slot0 = (size_t)bh * a.n_splits;
-    float mx = -INFINITY;
-    for (int s = 0; s < a.n_splits; ++s) mx = fmaxf(mx, a.ws_ml[(slot0 + s) * 2]);
-    float num = 0.f, den = 0.f;
-    for (int s = 0; s < a.n_splits; ++s) {
-        const float ms = a.ws_ml[(slot0 + s) * 2];
-        const float w = ms == -INFINITY ? 0.f : exp2f(ms - mx);
-        den += w * a.ws_ml[(slot0 + s) * 2 + 1];
-        num += w * a.ws_o[(slot0 + s) * HD + d];
+    // the (max, sum) pairs and this dimension of every split's partial are
+    // loaded together, four splits at a time, then merged in split order
+    constexpr int C = 4;
+    float mx = -INFINITY, num = 0.f, den = 0.f;
+    auto load = [&](int s0, float2* ml, float* o) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const bool in = s0 + c < a.n_splits;
+            ml[c] = in ? reinterpret_cast<const float2*>(a.ws_ml)[slot0 + s0 + c] : make_float2(-INFINITY, 0.f);
+            o[c] = in ? a.ws_o[(slot0 + s0 + c) * HD + d] : 0.f;
+        }
+    };
+    auto merge = [&](const float2* ml, const float* o) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const float w = ml[c].x == -INFINITY ? 0.f : exp2f(ml[c].x - mx);
+            den += w * ml[c].y;
+            num += w * o[c];
+        }
+    };
+    if (a.n_splits <= C) {
+        // the common case: every load in flight at once
+        float2 ml[C];
+        float o[C];
+        load(0, ml, o);
+#pragma unroll
+        for (int c = 0; c < C; ++c) mx = fmaxf(mx, ml[c].x);
+        merge(ml, o);
+    } else {
+        for (int s0 = 0; s0 < a.n_splits; s0 += C) {
+            float2 ml[C];
+            float o[C];
+            load(s0, ml, o);
+#pragma unroll
+            for (int c = 0; c < C; ++c) mx = fmaxf(mx, ml[c].x);
+        }
+        for (int s0 = 0; s0 < a.n_splits; s0 += C) {
+            float2 ml[C];
+            float o[C];
+            load(s0, ml, o);
+            merge(ml, o);
+        }
     }
     const int row = a.cu_q[b];
     if (row < 0 || row >= a.lse_rows) return;
